@@ -1,0 +1,187 @@
+/*
+ * tide.h -- C ABI of the paged-KV resume-attention library for AMD MI355X (gfx950).
+ *
+ * What the library computes (TideRL, arXiv 2608.10402):
+ *   A multi-turn agent task pauses while the environment runs, then resumes with
+ *   a longer context.  When the task's KV cache was kept resident (Continuous Task
+ *   Batching, Section 4, and its resume-with-cache-locality rule in Section 4.2),
+ *   the resume only has to run attention for the newly appended observation/action
+ *   tokens against the retained prefix.  When the cache was evicted (challenge C1
+ *   in Section 2.2) or invalidated by a weight update ("cache-free task migration",
+ *   Section 5.2), the whole history is prefilled again.  Between environment turns
+ *   the task decodes its next action one token at a time (Section 2.1).
+ *
+ *   The four compute entry points below are exactly these steps:
+ *     tide_kv_append          write new tokens' K/V into the shared page pool
+ *     tide_extend_attn        attention of the new tokens over retained prefix + themselves
+ *     tide_decode_attn        one query token per task over its whole context (split-K)
+ *     tide_full_prefill_attn  causal attention over the whole sequence (the recompute path)
+ *
+ *   The attention itself is standard scaled dot-product attention (Vaswani et al.,
+ *   2017), which the paper uses but does not restate: for a query row at absolute
+ *   position t of task b and query head h,
+ *       s_p = sm_scale * <q, k_p>           for key positions p = 0 .. t
+ *       o   = sum_p softmax(s)_p * v_p,     lse = log(sum_p exp(s_p))  (natural log)
+ *   with k_p, v_p taken from KV head floor(h / G), G = num_q_heads / num_kv_heads
+ *   (grouped-query attention).  Causality is bottom-right aligned: the j-th new token
+ *   of a task with prefix length P sits at position P + j and sees keys 0 .. P + j.
+ *
+ * Memory layout (all device buffers are owned by the caller):
+ *   element type     bf16 (raw 16-bit brain-float bit patterns) for Q, K, V, O;
+ *                    fp32 for LSE.
+ *   k_pool           bf16 [num_pages][num_kv_heads][page_size][head_dim]
+ *                    (one (page, kv-head) block is page_size rows of head_dim contiguous)
+ *   v_pool           bf16 [num_pages][num_kv_heads][head_dim][page_size]
+ *                    (V is stored transposed inside each page: for one head-dim index the
+ *                    page_size token slots are contiguous)
+ *   block_table      int32 [num_tasks][bt_stride], row-major, device memory.  Entry i of
+ *                    row b is the physical page holding logical positions
+ *                    [i*page_size, (i+1)*page_size) of task b.  Only the first
+ *                    ceil(len_b / page_size) entries of a row are read.
+ *   token tensors    packed ragged rows: task b owns rows [indptr_b, indptr_{b+1}) where
+ *                    indptr is the exclusive prefix sum of the per-task token counts in
+ *                    task order.  q/out: bf16 [rows][num_q_heads][head_dim];
+ *                    k_new/v_new: bf16 [rows][num_kv_heads][head_dim];
+ *                    lse: fp32 [rows][num_q_heads] (may be NULL).
+ *   lengths          HOST arrays of int32, read synchronously during the call (the
+ *                    scheduler that owns task footprints lives on the host, Section 4.1).
+ *   workspace        device scratch owned by the caller, at least tide_workspace_size()
+ *                    bytes; it must not be shared by two calls in flight at once.
+ *   stream           a hipStream_t passed as void*; NULL means the default stream.
+ *
+ * Supported shapes: head_dim in {64, 128}; page_size == 16; num_q_heads a multiple of
+ * num_kv_heads with G = num_q_heads / num_kv_heads in [1, 16].  Anything else returns
+ * TIDE_ERR_UNSUPPORTED.
+ *
+ * Semantics guaranteed by every attention entry point:
+ *   - Pool slots at or beyond a task's current length, and pages not listed in its
+ *     block-table prefix, never influence the result, even if they hold NaN or Inf.
+ *   - The result does not depend on which physical pages hold the data (bitwise, for a
+ *     fixed split count), and repeated calls on the same inputs are bitwise identical.
+ *   - A physical page id outside [0, num_pages) is never dereferenced: the kernels
+ *     skip it and set an error flag in the workspace; with the environment variable
+ *     TIDE_DEBUG_CHECKS=1 the call synchronizes the stream and returns
+ *     TIDE_ERR_PAGE_RANGE when the flag is set.
+ *
+ * Calls enqueue work on `stream` and return without synchronizing (except under
+ * TIDE_DEBUG_CHECKS=1).  Device faults surface at the caller's next synchronization.
+ * No C++ exception or abort crosses this interface.  The library never allocates
+ * device memory; it keeps a small pinned host staging ring (created lazily, released
+ * by tide_shutdown) to upload the per-call work lists.  Calls are thread-safe.
+ */
+#ifndef TIDE_H_
+#define TIDE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every entry point. */
+enum {
+  TIDE_OK = 0,
+  TIDE_ERR_INVALID_ARG = -1, /* null pointer, non-positive dimension, negative length */
+  TIDE_ERR_UNSUPPORTED = -2, /* head_dim / page_size / GQA ratio outside the supported set */
+  TIDE_ERR_CAPACITY = -3,    /* ceil(len/page_size) > bt_stride, or workspace too small */
+  TIDE_ERR_HIP = -4,         /* a HIP runtime call or kernel launch failed */
+  TIDE_ERR_PAGE_RANGE = -5   /* a block-table page id was outside [0, num_pages) (debug mode) */
+};
+
+/* Operation selector for tide_workspace_size. */
+enum {
+  TIDE_OP_KV_APPEND = 1,
+  TIDE_OP_EXTEND = 2,
+  TIDE_OP_DECODE = 3,
+  TIDE_OP_FULL_PREFILL = 4
+};
+
+/* Attention shape shared by all calls. */
+typedef struct tide_dims {
+  int32_t num_q_heads;  /* Hq */
+  int32_t num_kv_heads; /* Hkv; Hq % Hkv == 0 */
+  int32_t head_dim;     /* d: 64 or 128 */
+  int32_t page_size;    /* tokens per page: 16 */
+  float sm_scale;       /* softmax scale, usually 1/sqrt(d); must be finite and > 0 */
+} tide_dims;
+
+/*
+ * Bytes of device workspace the operation needs for these host lengths.
+ *   op == TIDE_OP_KV_APPEND / TIDE_OP_EXTEND: lens_a = prefix_lens, lens_b = extend_lens
+ *   op == TIDE_OP_DECODE:                     lens_a = kv_lens,     lens_b ignored
+ *   op == TIDE_OP_FULL_PREFILL:               lens_a = seq_lens,    lens_b ignored
+ * num_splits is used by TIDE_OP_DECODE only (0 = automatic; see tide_decode_attn).
+ * The size depends only on the arguments, never on device state.
+ */
+int tide_workspace_size(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* lens_b,
+                        const tide_dims* dims, int32_t num_splits, size_t* bytes_out);
+
+/*
+ * KV-append: store the K/V of each task's new tokens into its pages (the retained
+ * state that Continuous Task Batching keeps resident, Section 4).
+ * For task b, new token j (0 <= j < extend_lens[b]) sits at position
+ * pos = prefix_lens[b] + j and row r = indptr_b + j of k_new/v_new; for every KV head g:
+ *     k_pool[BT[b][pos/16]][g][pos%16][:] = k_new[r][g][:]
+ *     v_pool[BT[b][pos/16]][g][:][pos%16] = v_new[r][g][:]
+ * The copy is bit-exact; no other pool byte is written.  Two tasks must not map the
+ * same (page, slot); if they do, the result for that slot is unspecified.
+ */
+int tide_kv_append(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                   int64_t num_pages, const int32_t* block_table, int32_t bt_stride,
+                   int32_t num_tasks, const int32_t* prefix_lens, const int32_t* extend_lens,
+                   const tide_dims* dims, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Extend attention: resume of tasks whose KV was retained (Section 4.2; the cache hit
+ * that avoids the recompute of challenge C1, Section 2.2).  For each task b the
+ * extend_lens[b] query rows at positions prefix_lens[b] .. prefix_lens[b]+extend_lens[b]-1
+ * attend causally to keys 0 .. their own position, read from the pool only: the new
+ * tokens' K/V must already have been appended.  q/out rows are packed by extend_lens.
+ * extend_lens[b] == 0 contributes no rows; prefix_lens[b] == 0 is a fresh prefill.
+ */
+int tide_extend_attn(const void* q, const void* k_pool, const void* v_pool, int64_t num_pages,
+                     const int32_t* block_table, int32_t bt_stride, int32_t num_tasks,
+                     const int32_t* prefix_lens, const int32_t* extend_lens,
+                     const tide_dims* dims, void* out, float* lse, void* workspace,
+                     size_t workspace_bytes, void* stream);
+
+/*
+ * Decode attention: one query token per task (the action tokens generated between
+ * environment turns, Section 2.1) over its whole context of kv_lens[b] >= 1 positions,
+ * which include the token itself (append it first).  q/out: bf16 [num_tasks][Hq][d];
+ * lse: fp32 [num_tasks][Hq] or NULL.  The context is split into chunks processed in
+ * parallel and merged by log-sum-exp weights (split-K).  num_splits == 0 chooses the
+ * chunk size automatically; num_splits > 0 caps the number of chunks per task at that
+ * value.  Results for different split counts agree to fp32 rounding.
+ */
+int tide_decode_attn(const void* q, const void* k_pool, const void* v_pool, int64_t num_pages,
+                     const int32_t* block_table, int32_t bt_stride, int32_t num_tasks,
+                     const int32_t* kv_lens, const tide_dims* dims, int32_t num_splits,
+                     void* out, float* lse, void* workspace, size_t workspace_bytes,
+                     void* stream);
+
+/*
+ * Full re-prefill attention: causal attention over all seq_lens[b] positions of each
+ * task, the recomputation an evicted or invalidated cache forces (challenge C1,
+ * Section 2.2; fresh prefill after a weight sync, Section 5.2).  Identical to
+ * tide_extend_attn with prefix_lens = 0 and extend_lens = seq_lens.
+ */
+int tide_full_prefill_attn(const void* q, const void* k_pool, const void* v_pool,
+                           int64_t num_pages, const int32_t* block_table, int32_t bt_stride,
+                           int32_t num_tasks, const int32_t* seq_lens, const tide_dims* dims,
+                           void* out, float* lse, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/* Human-readable text for a status code (static storage, never NULL). */
+const char* tide_status_string(int status);
+
+/* Release the pinned host staging ring.  Safe to call at any time when no call is in
+ * flight on another thread; later calls recreate it. */
+void tide_shutdown(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TIDE_H_ */

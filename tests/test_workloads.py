@@ -1,0 +1,75 @@
+"""The seeded input generator: determinism, slicing, distribution, shapes (CPU only)."""
+import hashlib
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+
+def test_philox_known_answers():
+    # Known-answer vectors of Philox4x32-10 published with the Random123 library.
+    assert W.philox4x32_10((0, 0, 0, 0), (0, 0)) == [0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8]
+    assert W.philox4x32_10((0xFFFFFFFF,) * 4, (0xFFFFFFFF, 0xFFFFFFFF)) == [
+        0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD]
+    assert W.philox4x32_10((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344),
+                           (0xA4093822, 0x299F31D0)) == [0xD16CFE09, 0x94FDCCEB, 0x5001E420,
+                                                         0x24126EA1]
+
+
+def test_normal_distribution():
+    x = W.normal_f32(123, 1, 2, 0, 1 << 20).astype(np.float64)
+    assert abs(x.mean()) < 5e-3 and abs(x.std() - 1) < 5e-3
+    assert abs((np.abs(x) > 2).mean() - 0.0455) < 2e-3
+
+
+def test_slices_are_consistent():
+    a = W.normal_bf16(7, 2, 3, 0, 10007)
+    b = W.normal_bf16(7, 2, 3, 4093, 311)
+    assert np.array_equal(a[4093:4093 + 311], b)
+    wl = W.make_workload("tiny_extend")
+    full = wl.k_rows(2, 0, int(wl.seq_lens[2]))
+    assert np.array_equal(full[250:270], wl.k_rows(2, 250, 270))
+
+
+@pytest.mark.parametrize("key", sorted(W.SPECS))
+def test_workload_shapes(key):
+    wl = W.make_workload(key)
+    s = wl.spec
+    assert wl.prefix_lens.shape == (s.num_tasks,) and wl.extend_lens.shape == (s.num_tasks,)
+    final = wl.final_lens
+    used = []
+    for b in range(s.num_tasks):
+        n = -(-int(final[b]) // 16)
+        row = wl.block_table[b]
+        assert (row[:n] >= 0).all() and (row[:n] < wl.num_pages).all()
+        assert (row[n:] == -1).all()
+        used.extend(row[:n].tolist())
+    assert len(used) == len(set(used)), "a physical page is shared by two tasks"
+    if key == "tiny_extend":
+        assert wl.prefix_lens.tolist() == [37, 100, 250, 511]
+        assert wl.extend_lens.tolist() == [5, 17, 64, 128] and wl.num_pages == 128
+    if key == "agent_resume_7b":
+        assert wl.prefix_lens.min() >= 2048 and wl.prefix_lens.max() <= 16384
+        assert wl.extend_lens.min() >= 64 and wl.extend_lens.max() <= 2048
+    if key == "resumed_decode":
+        ctx = wl.seq_lens
+        assert ctx.min() >= 1024 and ctx.max() <= 32768 and (wl.extend_lens == 1).all()
+        assert 5000 < np.median(ctx) < 7500
+    if key == "multimodal_resume":
+        assert wl.extend_lens.min() >= 1024 and wl.extend_lens.max() <= 4096
+        frac = np.mean(np.concatenate(wl.outliers))
+        assert 0.09 < frac < 0.11
+    if key == "long_horizon":
+        pref_pages = sum(-(-int(p) // 16) for p in wl.prefix_lens)
+        assert abs(pref_pages / wl.num_pages - 0.9) < 1e-3
+
+
+def test_determinism_digest():
+    a = W.make_workload("agent_resume_7b")
+    b = W.make_workload("agent_resume_7b")
+    assert a.lens_digest() == b.lens_digest()
+    assert np.array_equal(a.block_table, b.block_table)
+    h1 = hashlib.sha256(a.q_rows(5, 100, 140).tobytes()).hexdigest()
+    h2 = hashlib.sha256(b.q_rows(5, 100, 140).tobytes()).hexdigest()
+    assert h1 == h2

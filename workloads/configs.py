@@ -1,0 +1,364 @@
+"""Seeded synthetic workloads shaped like multi-turn agentic rollouts.
+
+The paper measures on WebShop, AlfWorld, OSWorld and ScienceBoard trajectories
+(Section 6.1; per-workload turn and token counts in the task-statistics table of
+Appendix C).  Those datasets are not available here, and the attention path only
+needs their shapes, so every workload below is synthetic: lengths drawn from the
+stated laws, Q/K/V ~ N(0,1) rounded to bf16, and physical pages scattered over a
+shared pool.  The five workloads are:
+
+  tiny_extend        4 tasks, 8 q / 2 kv heads, d=64; fixed prefix/extend lengths
+  agent_resume_7b    64 tasks, 28 q / 4 kv heads (7B-class layer), d=128; prefix
+                     U{2048..16384}, extend (observation) log-uniform 64..2048
+  resumed_decode     256 tasks, 32 q / 8 kv heads, d=128; context lognormal
+                     (median 6144, sigma 0.7) clipped to [1024, 32768]; one token each
+  multimodal_resume  32 tasks, 32 q / 8 kv heads, d=128; prefix U{4096..24576},
+                     extend U{1024..4096}; K rows x4 on 10% of positions
+  long_horizon       32 tasks, 64 q / 8 kv heads, d=128; prefix U{32768..98304},
+                     extend U{256..1024}; pool 90% occupied; then 8 decode steps
+
+This module only draws inputs (lengths, page placement, tensor values); it holds
+none of the attention arithmetic.
+"""
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import _native
+
+# Stream ids of the counter-based generator (stream_a); stream_b is the task index.
+TENSOR_Q = 1
+TENSOR_K = 2
+TENSOR_V = 3
+
+KILO = 1024  # "2k", "16k", "96k" ... are read as multiples of 1024
+
+
+@dataclass(frozen=True)
+class Spec:
+    key: str
+    index: int
+    text: str
+    num_tasks: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    page_size: int
+    kind: str  # "extend" | "decode" | "long_horizon"
+    prefix: tuple = ()  # ("fixed", values) | ("uniform", lo, hi)
+    extend: tuple = ()  # ("fixed", values) | ("uniform", lo, hi) | ("loguniform", lo, hi)
+    context: tuple = ()  # decode only: ("lognormal", median, sigma, lo, hi)
+    pool: tuple = ("fragmented", 1.1)  # ("perm", N) | ("fragmented", f) | ("occupied", f)
+    outlier_frac: float = 0.0
+    outlier_scale: float = 1.0
+    decode_steps: int = 0
+    salt: int = 0  # 0 for the full-size workload; shrunken variants use their own seeds
+
+    @property
+    def group(self) -> int:
+        return self.num_q_heads // self.num_kv_heads
+
+    def shrunk(self, num_tasks: int, length_div: int, salt: int = 1) -> "Spec":
+        """A smaller workload with the same structure, for CPU-sized oracle checks."""
+
+        def div_range(law):
+            if not law:
+                return law
+            if law[0] == "fixed":
+                return ("fixed", tuple(max(1, v // length_div) for v in law[1][:num_tasks]))
+            if law[0] in ("uniform", "loguniform"):
+                return (law[0], max(1, law[1] // length_div), max(1, law[2] // length_div))
+            if law[0] == "lognormal":
+                return ("lognormal", max(2, law[1] // length_div), law[2],
+                        max(2, law[3] // length_div), max(2, law[4] // length_div))
+            raise ValueError(law)
+
+        pool = self.pool
+        if pool[0] == "perm":
+            pool = ("fragmented", 1.5)
+        return dataclasses.replace(
+            self, num_tasks=num_tasks, prefix=div_range(self.prefix),
+            extend=div_range(self.extend), context=div_range(self.context), pool=pool,
+            salt=salt)
+
+
+SPECS = {
+    "tiny_extend": Spec(
+        key="tiny_extend", index=1,
+        text=("Tiny extend-attention: 4 tasks, 8 query heads / 2 KV heads (GQA), head_dim 64, "
+              "page size 16, prefix lens {37,100,250,511}, extend lens {5,17,64,128}, causal; "
+              "Q/K/V bf16 ~ N(0,1), softmax scale 1/sqrt(64); physical pages a seeded random "
+              "permutation of a 128-page pool"),
+        num_tasks=4, num_q_heads=8, num_kv_heads=2, head_dim=64, page_size=16, kind="extend",
+        prefix=("fixed", (37, 100, 250, 511)), extend=("fixed", (5, 17, 64, 128)),
+        pool=("perm", 128)),
+    "agent_resume_7b": Spec(
+        key="agent_resume_7b", index=2,
+        text=("Agent resume, 7B-class layer: 64 tasks, 28 query / 4 KV heads, head_dim 128, "
+              "page 16, prefix lens uniform 2k-16k, extend (observation) lens log-uniform "
+              "64-2048, bf16 ~ N(0,1), causal, fragmented random page placement; also full "
+              "re-prefill of the same sequences for comparison"),
+        num_tasks=64, num_q_heads=28, num_kv_heads=4, head_dim=128, page_size=16, kind="extend",
+        prefix=("uniform", 2 * KILO, 16 * KILO), extend=("loguniform", 64, 2048),
+        pool=("fragmented", 1.1)),
+    "resumed_decode": Spec(
+        key="resumed_decode", index=3,
+        text=("Resumed decode: 256 concurrent tasks, 1 query token each, 32 query / 8 KV heads, "
+              "head_dim 128, page 16, context lens lognormal (median 6k, clipped 1k-32k), "
+              "bf16 ~ N(0,1), split-K over context"),
+        num_tasks=256, num_q_heads=32, num_kv_heads=8, head_dim=128, page_size=16, kind="decode",
+        context=("lognormal", 6 * KILO, 0.7, 1 * KILO, 32 * KILO), pool=("fragmented", 1.1)),
+    "multimodal_resume": Spec(
+        key="multimodal_resume", index=4,
+        text=("Multi-modal observation resume: 32 tasks, 32 query / 8 KV heads, head_dim 128, "
+              "page 16, prefix lens uniform 4k-24k, extend lens uniform 1024-4096 "
+              "(image-patch-sized chunks), bf16 with K rows scaled x4 on 10% of positions "
+              "(outlier tokens), causal"),
+        num_tasks=32, num_q_heads=32, num_kv_heads=8, head_dim=128, page_size=16, kind="extend",
+        prefix=("uniform", 4 * KILO, 24 * KILO), extend=("uniform", 1024, 4096),
+        pool=("fragmented", 1.1), outlier_frac=0.1, outlier_scale=4.0),
+    "long_horizon": Spec(
+        key="long_horizon", index=5,
+        text=("Long-horizon agent: 32 tasks, 64 query / 8 KV heads, head_dim 128, page 16, "
+              "prefix lens uniform 32k-96k, extend lens uniform 256-1024, bf16 ~ N(0,1); "
+              "KV-append of extend tokens into a 90%-occupied shuffled page pool, followed by "
+              "extend-attention and then 8 decode steps per task"),
+        num_tasks=32, num_q_heads=64, num_kv_heads=8, head_dim=128, page_size=16,
+        kind="long_horizon", prefix=("uniform", 32 * KILO, 96 * KILO), extend=("uniform", 256, 1024),
+        pool=("occupied", 0.9), decode_steps=8),
+}
+
+
+def _ceil_div(a, b):
+    return -(-a // b)
+
+
+@dataclass
+class Workload:
+    """Drawn lengths, page placement and lazily generated tensors of one workload.
+
+    Positions of task b: 0 .. prefix_lens[b]-1 are the retained prefix,
+    prefix_lens[b] .. prefix_lens[b]+extend_lens[b]-1 the resumed (appended) tokens, and
+    for long_horizon the next decode_steps positions are the decoded tokens.
+    """
+
+    spec: Spec
+    prefix_lens: np.ndarray
+    extend_lens: np.ndarray
+    block_table: np.ndarray
+    num_pages: int
+    seeds: dict
+    outliers: list = field(default_factory=list)
+
+    # ---- shape helpers -------------------------------------------------------------
+    @property
+    def num_tasks(self):
+        return self.spec.num_tasks
+
+    @property
+    def seq_lens(self) -> np.ndarray:
+        return (self.prefix_lens + self.extend_lens).astype(np.int32)
+
+    @property
+    def final_lens(self) -> np.ndarray:
+        return (self.seq_lens + self.spec.decode_steps).astype(np.int32)
+
+    @property
+    def sm_scale(self) -> float:
+        return 1.0 / math.sqrt(self.spec.head_dim)
+
+    @property
+    def bt_stride(self) -> int:
+        return int(self.block_table.shape[1])
+
+    def lens_digest(self) -> str:
+        h = hashlib.sha256()
+        h.update(self.prefix_lens.astype("<i4").tobytes())
+        h.update(self.extend_lens.astype("<i4").tobytes())
+        return h.hexdigest()[:16]
+
+    # ---- tensor slices (bf16 bit patterns as uint16) --------------------------------
+    def _rows(self, tensor: int, heads: int, b: int, t0: int, t1: int, out=None) -> np.ndarray:
+        d = self.spec.head_dim
+        rows = max(0, t1 - t0)
+        flat = None if out is None else out.reshape(-1)
+        flat = _native.normal_bf16(self.seeds[tensor], tensor, b, t0 * heads * d,
+                                   rows * heads * d, out=flat)
+        return flat.reshape(rows, heads, d)
+
+    def q_rows(self, b: int, t0: int, t1: int, out=None) -> np.ndarray:
+        return self._rows(TENSOR_Q, self.spec.num_q_heads, b, t0, t1, out)
+
+    def k_rows(self, b: int, t0: int, t1: int, out=None) -> np.ndarray:
+        k = self._rows(TENSOR_K, self.spec.num_kv_heads, b, t0, t1, out)
+        if self.outliers:
+            sel = self.outliers[b][t0:t1]
+            if sel.any():
+                f = _bf16_to_f32(k[sel]) * np.float32(self.spec.outlier_scale)
+                k[sel] = _f32_to_bf16_exact(f)
+        return k
+
+    def v_rows(self, b: int, t0: int, t1: int, out=None) -> np.ndarray:
+        return self._rows(TENSOR_V, self.spec.num_kv_heads, b, t0, t1, out)
+
+    def packed(self, which: str, ranges) -> np.ndarray:
+        """Concatenate per-task row ranges [(t0, t1)] of 'q', 'k' or 'v' in task order."""
+        fn = {"q": self.q_rows, "k": self.k_rows, "v": self.v_rows}[which]
+        heads = self.spec.num_q_heads if which == "q" else self.spec.num_kv_heads
+        total = sum(max(0, t1 - t0) for t0, t1 in ranges)
+        out = np.empty((total, heads, self.spec.head_dim), dtype=np.uint16)
+        row = 0
+        for b, (t0, t1) in enumerate(ranges):
+            n = max(0, t1 - t0)
+            if n:
+                fn(b, t0, t1, out=out[row:row + n])
+            row += n
+        return out
+
+    def prefix_ranges(self):
+        return [(0, int(p)) for p in self.prefix_lens]
+
+    def extend_ranges(self):
+        return [(int(p), int(p + e)) for p, e in zip(self.prefix_lens, self.extend_lens)]
+
+    def full_ranges(self):
+        return [(0, int(l)) for l in self.seq_lens]
+
+    def decode_ranges(self, step: int):
+        return [(int(l) + step, int(l) + step + 1) for l in self.seq_lens]
+
+    def remap_pages(self, perm: np.ndarray) -> "Workload":
+        """The same workload with physical page i moved to page perm[i]."""
+        bt = self.block_table.copy()
+        live = bt >= 0
+        bt[live] = perm[bt[live]]
+        return dataclasses.replace(self, block_table=bt)
+
+
+def _bf16_to_f32(a: np.ndarray) -> np.ndarray:
+    return (a.astype(np.uint32) << 16).view(np.float32)
+
+
+def _f32_to_bf16_exact(f: np.ndarray) -> np.ndarray:
+    u = f.astype(np.float32).view(np.uint32)
+    assert not (u & 0xFFFF).any(), "scaled value is not exactly representable in bf16"
+    return (u >> 16).astype(np.uint16)
+
+
+def _draw_lengths(spec: Spec, rng: np.random.Generator):
+    b = spec.num_tasks
+    if spec.kind == "decode":
+        law = spec.context
+        assert law[0] == "lognormal"
+        _, median, sigma, lo, hi = law
+        ctx = np.rint(rng.lognormal(math.log(median), sigma, size=b))
+        ctx = np.clip(ctx, lo, hi).astype(np.int64)
+        # the newest token of each task is the one being decoded: it is appended first
+        return (ctx - 1).astype(np.int32), np.ones(b, dtype=np.int32)
+
+    def draw(law):
+        if law[0] == "fixed":
+            vals = np.asarray(law[1][:b], dtype=np.int64)
+            assert vals.size == b
+            return vals
+        if law[0] == "uniform":
+            return rng.integers(law[1], law[2], size=b, endpoint=True)
+        if law[0] == "loguniform":
+            lo, hi = law[1], law[2]
+            v = np.floor(np.exp(rng.uniform(math.log(lo), math.log(hi), size=b)))
+            return np.clip(v, lo, hi).astype(np.int64)
+        raise ValueError(law)
+
+    p = draw(spec.prefix)
+    e = draw(spec.extend)
+    return p.astype(np.int32), e.astype(np.int32)
+
+
+def _place_pages(spec: Spec, prefix, extend, rng: np.random.Generator):
+    ps = spec.page_size
+    final = prefix.astype(np.int64) + extend + spec.decode_steps
+    need = [_ceil_div(int(f), ps) for f in final]
+    stride = max(1, max(need) if need else 1)
+    bt = np.full((spec.num_tasks, stride), -1, dtype=np.int32)
+    kind = spec.pool[0]
+    if kind in ("perm", "fragmented"):
+        total = int(sum(need))
+        n = spec.pool[1] if kind == "perm" else int(math.ceil(spec.pool[1] * total))
+        assert n >= total, "pool too small"
+        perm = rng.permutation(n).astype(np.int32)
+        at = 0
+        for b, k in enumerate(need):
+            bt[b, :k] = perm[at:at + k]
+            at += k
+        return bt, n
+    if kind == "occupied":
+        pref_pages = [_ceil_div(int(p), ps) for p in prefix]
+        n_pref = int(sum(pref_pages))
+        n = int(math.ceil(n_pref / spec.pool[1]))
+        perm = rng.permutation(n).astype(np.int32)
+        at = 0
+        for b, k in enumerate(pref_pages):
+            bt[b, :k] = perm[at:at + k]
+            at += k
+        free = list(perm[at:])
+        free.reverse()  # pop() takes from the front of the shuffled free list
+        # the appended tokens first fill each task's partial last page, then take free pages
+        for b in range(spec.num_tasks):
+            for lp in range(pref_pages[b], _ceil_div(int(prefix[b] + extend[b]), ps)):
+                bt[b, lp] = free.pop()
+        # decode steps, one token per task per step, in task order
+        for s in range(spec.decode_steps):
+            for b in range(spec.num_tasks):
+                pos = int(prefix[b] + extend[b]) + s
+                if pos % ps == 0:
+                    bt[b, pos // ps] = free.pop()
+        return bt, n
+    raise ValueError(spec.pool)
+
+
+def make_workload(spec: Spec | str) -> Workload:
+    """Draw one workload.  Same spec => same lengths, pages and tensor values."""
+    if isinstance(spec, str):
+        spec = SPECS[spec]
+    ss = np.random.SeedSequence([2608, 10402, spec.index, spec.salt])
+    c_lens, c_pages, c_q, c_k, c_v, c_out = ss.spawn(6)
+    prefix, extend = _draw_lengths(spec, np.random.Generator(np.random.PCG64(c_lens)))
+    bt, n_pages = _place_pages(spec, prefix, extend, np.random.Generator(np.random.PCG64(c_pages)))
+
+    def seed64(c):
+        w = c.generate_state(2, np.uint32)
+        return int(w[0]) | (int(w[1]) << 32)
+
+    seeds = {TENSOR_Q: seed64(c_q), TENSOR_K: seed64(c_k), TENSOR_V: seed64(c_v)}
+    outliers = []
+    if spec.outlier_frac > 0:
+        rng = np.random.Generator(np.random.PCG64(c_out))
+        final = prefix.astype(np.int64) + extend + spec.decode_steps
+        outliers = [rng.random(int(f)) < spec.outlier_frac for f in final]
+    return Workload(spec=spec, prefix_lens=prefix, extend_lens=extend, block_table=bt,
+                    num_pages=int(n_pages), seeds=seeds, outliers=outliers)
+
+
+def custom_workload(num_q_heads: int, num_kv_heads: int, head_dim: int, prefix_lens,
+                    extend_lens, num_pages: int | None = None, seed: int = 0,
+                    decode_steps: int = 0, outlier_frac: float = 0.0) -> Workload:
+    """A workload with explicit lengths (edge cases: empty extends, fresh tasks, ...)."""
+    prefix = np.asarray(prefix_lens, dtype=np.int32)
+    extend = np.asarray(extend_lens, dtype=np.int32)
+    spec = Spec(key="custom", index=100 + seed, text="explicit lengths", num_tasks=int(prefix.size),
+                num_q_heads=num_q_heads, num_kv_heads=num_kv_heads, head_dim=head_dim,
+                page_size=16, kind="extend", prefix=("fixed", tuple(int(x) for x in prefix)),
+                extend=("fixed", tuple(int(x) for x in extend)),
+                pool=("fragmented", 1.25) if num_pages is None else ("perm", num_pages),
+                decode_steps=decode_steps, outlier_frac=outlier_frac,
+                outlier_scale=4.0 if outlier_frac else 1.0, salt=seed)
+    if num_pages is not None:
+        need = sum(_ceil_div(int(p + e + decode_steps), 16) for p, e in zip(prefix, extend))
+        if need > num_pages:
+            spec = dataclasses.replace(spec, pool=("fragmented", 1.25))
+    return make_workload(spec)
