@@ -75,6 +75,12 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#if defined(__GNUC__) || defined(__clang__)
+#define TIDE_API __attribute__((visibility("default")))
+#else
+#define TIDE_API
+#endif
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -114,7 +120,7 @@ typedef struct tide_dims {
  * num_splits is used by TIDE_OP_DECODE only (0 = automatic; see tide_decode_attn).
  * The size depends only on the arguments, never on device state.
  */
-int tide_workspace_size(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* lens_b,
+TIDE_API int tide_workspace_size(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* lens_b,
                         const tide_dims* dims, int32_t num_splits, size_t* bytes_out);
 
 /*
@@ -127,7 +133,7 @@ int tide_workspace_size(int op, int32_t num_tasks, const int32_t* lens_a, const 
  * The copy is bit-exact; no other pool byte is written.  Two tasks must not map the
  * same (page, slot); if they do, the result for that slot is unspecified.
  */
-int tide_kv_append(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+TIDE_API int tide_kv_append(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
                    int64_t num_pages, const int32_t* block_table, int32_t bt_stride,
                    int32_t num_tasks, const int32_t* prefix_lens, const int32_t* extend_lens,
                    const tide_dims* dims, void* workspace, size_t workspace_bytes, void* stream);
@@ -140,7 +146,7 @@ int tide_kv_append(const void* k_new, const void* v_new, void* k_pool, void* v_p
  * tokens' K/V must already have been appended.  q/out rows are packed by extend_lens.
  * extend_lens[b] == 0 contributes no rows; prefix_lens[b] == 0 is a fresh prefill.
  */
-int tide_extend_attn(const void* q, const void* k_pool, const void* v_pool, int64_t num_pages,
+TIDE_API int tide_extend_attn(const void* q, const void* k_pool, const void* v_pool, int64_t num_pages,
                      const int32_t* block_table, int32_t bt_stride, int32_t num_tasks,
                      const int32_t* prefix_lens, const int32_t* extend_lens,
                      const tide_dims* dims, void* out, float* lse, void* workspace,
@@ -155,7 +161,7 @@ int tide_extend_attn(const void* q, const void* k_pool, const void* v_pool, int6
  * chunk size automatically; num_splits > 0 caps the number of chunks per task at that
  * value.  Results for different split counts agree to fp32 rounding.
  */
-int tide_decode_attn(const void* q, const void* k_pool, const void* v_pool, int64_t num_pages,
+TIDE_API int tide_decode_attn(const void* q, const void* k_pool, const void* v_pool, int64_t num_pages,
                      const int32_t* block_table, int32_t bt_stride, int32_t num_tasks,
                      const int32_t* kv_lens, const tide_dims* dims, int32_t num_splits,
                      void* out, float* lse, void* workspace, size_t workspace_bytes,
@@ -167,18 +173,18 @@ int tide_decode_attn(const void* q, const void* k_pool, const void* v_pool, int6
  * Section 2.2; fresh prefill after a weight sync, Section 5.2).  Identical to
  * tide_extend_attn with prefix_lens = 0 and extend_lens = seq_lens.
  */
-int tide_full_prefill_attn(const void* q, const void* k_pool, const void* v_pool,
+TIDE_API int tide_full_prefill_attn(const void* q, const void* k_pool, const void* v_pool,
                            int64_t num_pages, const int32_t* block_table, int32_t bt_stride,
                            int32_t num_tasks, const int32_t* seq_lens, const tide_dims* dims,
                            void* out, float* lse, void* workspace, size_t workspace_bytes,
                            void* stream);
 
 /* Human-readable text for a status code (static storage, never NULL). */
-const char* tide_status_string(int status);
+TIDE_API const char* tide_status_string(int status);
 
 /* Release the pinned host staging ring.  Safe to call at any time when no call is in
  * flight on another thread; later calls recreate it. */
-void tide_shutdown(void);
+TIDE_API void tide_shutdown(void);
 
 #ifdef __cplusplus
 }

@@ -1,0 +1,218 @@
+"""ctypes binding of libtide.so: the entry points of include/tide.h under the same names.
+
+Argument marshalling only -- every step of the computation runs in the HIP kernels.
+Device buffers are torch tensors on a ROCm device (torch supplies memory and streams);
+lengths are host arrays.  Missing library => ImportError; a non-zero status from the
+library => TideError.  There is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtide.so")
+
+TIDE_OK = 0
+TIDE_ERR_INVALID_ARG = -1
+TIDE_ERR_UNSUPPORTED = -2
+TIDE_ERR_CAPACITY = -3
+TIDE_ERR_HIP = -4
+TIDE_ERR_PAGE_RANGE = -5
+
+TIDE_OP_KV_APPEND = 1
+TIDE_OP_EXTEND = 2
+TIDE_OP_DECODE = 3
+TIDE_OP_FULL_PREFILL = 4
+
+EXPORTED = ("tide_workspace_size", "tide_kv_append", "tide_extend_attn", "tide_decode_attn",
+            "tide_full_prefill_attn", "tide_status_string", "tide_shutdown")
+
+
+class TideError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s failed: %s (%d)" % (where, status_string(status), status))
+
+
+class tide_dims(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("sm_scale", ctypes.c_float)]
+
+
+def make_dims(num_q_heads: int, num_kv_heads: int, head_dim: int, sm_scale: float,
+              page_size: int = 16) -> tide_dims:
+    return tide_dims(num_q_heads, num_kv_heads, head_dim, page_size, sm_scale)
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libtide.so (once).  Raises ImportError when it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError("libtide.so not found at %s; build it with "
+                          "`python -m paper_2608_10402_amd.build`" % path)
+    lib = ctypes.CDLL(path)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    dims_p = ctypes.POINTER(tide_dims)
+    lib.tide_workspace_size.argtypes = [ctypes.c_int, i32, vp, vp, dims_p, i32,
+                                        ctypes.POINTER(sz)]
+    lib.tide_kv_append.argtypes = [vp, vp, vp, vp, i64, vp, i32, i32, vp, vp, dims_p, vp, sz, vp]
+    lib.tide_extend_attn.argtypes = [vp, vp, vp, i64, vp, i32, i32, vp, vp, dims_p, vp, vp, vp,
+                                     sz, vp]
+    lib.tide_decode_attn.argtypes = [vp, vp, vp, i64, vp, i32, i32, vp, dims_p, i32, vp, vp, vp,
+                                     sz, vp]
+    lib.tide_full_prefill_attn.argtypes = [vp, vp, vp, i64, vp, i32, i32, vp, dims_p, vp, vp, vp,
+                                           sz, vp]
+    for name in EXPORTED[:-2]:
+        getattr(lib, name).restype = ctypes.c_int
+    lib.tide_status_string.argtypes = [ctypes.c_int]
+    lib.tide_status_string.restype = ctypes.c_char_p
+    lib.tide_shutdown.argtypes = []
+    lib.tide_shutdown.restype = None
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().tide_status_string(int(status)).decode()
+
+
+# ---- marshalling helpers ------------------------------------------------------------------
+def _dev(t, dtype, name, nullable=False):
+    if t is None:
+        if nullable:
+            return None
+        raise ValueError("%s is required" % name)
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.device.type != "cuda":
+        raise ValueError("%s must live on a ROCm device" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return t.data_ptr() if t.numel() else None
+
+
+def _host(a, name):
+    if a is None:
+        return None, None
+    arr = np.ascontiguousarray(np.asarray(a), dtype=np.int32)
+    if arr.ndim != 1:
+        raise ValueError("%s must be 1-D" % name)
+    return arr, arr.ctypes.data
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _check(status, where):
+    if status != TIDE_OK:
+        raise TideError(status, where)
+
+
+def _ws(workspace):
+    if workspace is None:
+        return None, 0
+    if not isinstance(workspace, torch.Tensor) or workspace.device.type != "cuda":
+        raise ValueError("workspace must be a device tensor")
+    return workspace.data_ptr(), workspace.numel() * workspace.element_size()
+
+
+def _pool_shape(k_pool, v_pool, dims):
+    if k_pool.dim() != 4 or v_pool.dim() != 4:
+        raise ValueError("pools must be 4-D")
+    n, hkv, ps, d = k_pool.shape
+    if (hkv, ps, d) != (dims.num_kv_heads, dims.page_size, dims.head_dim):
+        raise ValueError("k_pool must be [num_pages][Hkv][page_size][d]")
+    if tuple(v_pool.shape) != (n, hkv, d, ps):
+        raise ValueError("v_pool must be [num_pages][Hkv][d][page_size]")
+    return int(n)
+
+
+# ---- entry points ---------------------------------------------------------------------------
+def tide_workspace_size(op: int, lens_a, lens_b, dims: tide_dims, num_splits: int = 0) -> int:
+    a, a_p = _host(lens_a, "lens_a")
+    b, b_p = _host(lens_b, "lens_b")
+    n = 0 if a is None else int(a.size)
+    out = ctypes.c_size_t(0)
+    _check(load().tide_workspace_size(op, n, a_p, b_p, ctypes.byref(dims), int(num_splits),
+                                      ctypes.byref(out)), "tide_workspace_size")
+    return int(out.value)
+
+
+def alloc_workspace(nbytes: int, device="cuda") -> torch.Tensor:
+    return torch.empty(max(1, int(nbytes)), dtype=torch.uint8, device=device)
+
+
+def tide_kv_append(k_new, v_new, k_pool, v_pool, block_table, prefix_lens, extend_lens,
+                   dims: tide_dims, workspace, stream=None) -> None:
+    num_pages = _pool_shape(k_pool, v_pool, dims)
+    p, p_p = _host(prefix_lens, "prefix_lens")
+    e, e_p = _host(extend_lens, "extend_lens")
+    ws, ws_n = _ws(workspace)
+    _check(load().tide_kv_append(
+        _dev(k_new, torch.bfloat16, "k_new"), _dev(v_new, torch.bfloat16, "v_new"),
+        _dev(k_pool, torch.bfloat16, "k_pool"), _dev(v_pool, torch.bfloat16, "v_pool"),
+        num_pages, _dev(block_table, torch.int32, "block_table"), int(block_table.shape[1]),
+        int(p.size), p_p, e_p, ctypes.byref(dims), ws, ws_n, _stream(stream)), "tide_kv_append")
+
+
+def tide_extend_attn(q, k_pool, v_pool, block_table, prefix_lens, extend_lens, dims: tide_dims,
+                     out, lse=None, workspace=None, stream=None) -> None:
+    num_pages = _pool_shape(k_pool, v_pool, dims)
+    p, p_p = _host(prefix_lens, "prefix_lens")
+    e, e_p = _host(extend_lens, "extend_lens")
+    ws, ws_n = _ws(workspace)
+    _check(load().tide_extend_attn(
+        _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"),
+        _dev(v_pool, torch.bfloat16, "v_pool"), num_pages,
+        _dev(block_table, torch.int32, "block_table"), int(block_table.shape[1]), int(p.size),
+        p_p, e_p, ctypes.byref(dims), _dev(out, torch.bfloat16, "out"),
+        _dev(lse, torch.float32, "lse", nullable=True), ws, ws_n, _stream(stream)),
+        "tide_extend_attn")
+
+
+def tide_decode_attn(q, k_pool, v_pool, block_table, kv_lens, dims: tide_dims, out, lse=None,
+                     num_splits: int = 0, workspace=None, stream=None) -> None:
+    num_pages = _pool_shape(k_pool, v_pool, dims)
+    kv, kv_p = _host(kv_lens, "kv_lens")
+    ws, ws_n = _ws(workspace)
+    _check(load().tide_decode_attn(
+        _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"),
+        _dev(v_pool, torch.bfloat16, "v_pool"), num_pages,
+        _dev(block_table, torch.int32, "block_table"), int(block_table.shape[1]), int(kv.size),
+        kv_p, ctypes.byref(dims), int(num_splits), _dev(out, torch.bfloat16, "out"),
+        _dev(lse, torch.float32, "lse", nullable=True), ws, ws_n, _stream(stream)),
+        "tide_decode_attn")
+
+
+def tide_full_prefill_attn(q, k_pool, v_pool, block_table, seq_lens, dims: tide_dims, out,
+                           lse=None, workspace=None, stream=None) -> None:
+    num_pages = _pool_shape(k_pool, v_pool, dims)
+    s, s_p = _host(seq_lens, "seq_lens")
+    ws, ws_n = _ws(workspace)
+    _check(load().tide_full_prefill_attn(
+        _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"),
+        _dev(v_pool, torch.bfloat16, "v_pool"), num_pages,
+        _dev(block_table, torch.int32, "block_table"), int(block_table.shape[1]), int(s.size),
+        s_p, ctypes.byref(dims), _dev(out, torch.bfloat16, "out"),
+        _dev(lse, torch.float32, "lse", nullable=True), ws, ws_n, _stream(stream)),
+        "tide_full_prefill_attn")
+
+
+def tide_shutdown() -> None:
+    load().tide_shutdown()

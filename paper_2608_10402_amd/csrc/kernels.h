@@ -1,0 +1,14 @@
+// Host-side launchers of the gfx950 kernels (one per .hip file).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "tide_common.h"
+
+namespace tide {
+
+hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
+hipError_t launch_extend(const ExtendArgs& a, int head_dim, int waves, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs& a, int head_dim, hipStream_t stream);
+
+}  // namespace tide

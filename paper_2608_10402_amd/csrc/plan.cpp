@@ -1,0 +1,227 @@
+// Host-side planning: validation, workspace layout and work lists (see plan.h).
+#include "plan.h"
+
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <numeric>
+
+namespace tide {
+
+int check_dims(const tide_dims* dims) {
+  if (!dims) return TIDE_ERR_INVALID_ARG;
+  if (dims->num_q_heads <= 0 || dims->num_kv_heads <= 0 || dims->head_dim <= 0 ||
+      dims->page_size <= 0)
+    return TIDE_ERR_INVALID_ARG;
+  if (!(dims->sm_scale > 0.0f) || !isfinite(dims->sm_scale)) return TIDE_ERR_INVALID_ARG;
+  if (dims->head_dim != 64 && dims->head_dim != 128) return TIDE_ERR_UNSUPPORTED;
+  if (dims->page_size != kPage) return TIDE_ERR_UNSUPPORTED;
+  if (dims->num_q_heads % dims->num_kv_heads != 0) return TIDE_ERR_UNSUPPORTED;
+  if (dims->num_q_heads / dims->num_kv_heads > kMaxGroup) return TIDE_ERR_UNSUPPORTED;
+  return TIDE_OK;
+}
+
+int32_t extend_waves(int32_t head_dim, int32_t group) {
+  (void)head_dim;
+  (void)group;
+  return 4;
+}
+
+namespace {
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Per-task (prefix, extend) of the positions this call touches or attends.
+int task_lengths(int op, int32_t b, const int32_t* lens_a, const int32_t* lens_b, int32_t* prefix,
+                 int32_t* extend) {
+  switch (op) {
+    case TIDE_OP_KV_APPEND:
+    case TIDE_OP_EXTEND:
+      *prefix = lens_a[b];
+      *extend = lens_b[b];
+      if (*prefix < 0 || *extend < 0) return TIDE_ERR_INVALID_ARG;
+      break;
+    case TIDE_OP_FULL_PREFILL:
+      *prefix = 0;
+      *extend = lens_a[b];
+      if (*extend < 0) return TIDE_ERR_INVALID_ARG;
+      break;
+    case TIDE_OP_DECODE:
+      if (lens_a[b] <= 0) return TIDE_ERR_INVALID_ARG;
+      *prefix = lens_a[b] - 1;
+      *extend = 1;
+      break;
+    default:
+      return TIDE_ERR_INVALID_ARG;
+  }
+  if ((int64_t)*prefix + *extend > INT32_MAX) return TIDE_ERR_INVALID_ARG;
+  return TIDE_OK;
+}
+
+}  // namespace
+
+int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* lens_b,
+              const tide_dims& dims, int32_t num_splits, int32_t bt_stride, bool build_blob,
+              Plan* plan) {
+  if (!plan) return TIDE_ERR_INVALID_ARG;
+  if (op != TIDE_OP_KV_APPEND && op != TIDE_OP_EXTEND && op != TIDE_OP_DECODE &&
+      op != TIDE_OP_FULL_PREFILL)
+    return TIDE_ERR_INVALID_ARG;
+  if (num_tasks < 0) return TIDE_ERR_INVALID_ARG;
+  if (num_tasks > 0 && !lens_a) return TIDE_ERR_INVALID_ARG;
+  if (num_tasks > 0 && (op == TIDE_OP_KV_APPEND || op == TIDE_OP_EXTEND) && !lens_b)
+    return TIDE_ERR_INVALID_ARG;
+  if (op == TIDE_OP_DECODE && num_splits < 0) return TIDE_ERR_INVALID_ARG;
+  int rc = check_dims(&dims);
+  if (rc != TIDE_OK) return rc;
+
+  const int32_t group = dims.num_q_heads / dims.num_kv_heads;
+  *plan = Plan();
+  plan->op = op;
+  plan->num_tasks = num_tasks;
+
+  std::vector<TaskDesc> tasks((size_t)num_tasks);
+  int64_t rows = 0;
+  int64_t max_len = 0;
+  for (int32_t b = 0; b < num_tasks; ++b) {
+    int32_t p = 0, e = 0;
+    rc = task_lengths(op, b, lens_a, lens_b, &p, &e);
+    if (rc != TIDE_OK) return rc;
+    tasks[b].row_start = (int32_t)(op == TIDE_OP_DECODE ? b : rows);
+    tasks[b].prefix = p;
+    tasks[b].extend = e;
+    tasks[b].aux = 0;
+    rows += (op == TIDE_OP_DECODE) ? 1 : e;
+    if (rows > INT32_MAX) return TIDE_ERR_INVALID_ARG;
+    max_len = std::max<int64_t>(max_len, (int64_t)p + e);
+    if (bt_stride >= 0 && ceil_div((int64_t)p + e, kPage) > bt_stride) return TIDE_ERR_CAPACITY;
+  }
+  plan->total_rows = (int32_t)rows;
+
+  // ---- work items -------------------------------------------------------------------
+  std::vector<uint8_t> items_bytes;
+  int64_t n_items = 0;
+  if (op == TIDE_OP_KV_APPEND) {
+    std::vector<AppendItem> items;
+    for (int32_t b = 0; b < num_tasks; ++b) {
+      const int32_t p = tasks[b].prefix, e = tasks[b].extend;
+      if (e == 0) continue;
+      for (int64_t lp = p / kPage; lp <= (int64_t)(p + e - 1) / kPage; ++lp) {
+        AppendItem it;
+        it.task = b;
+        it.lpage = (int32_t)lp;
+        it.pos_begin = (int32_t)std::max<int64_t>(p, lp * kPage);
+        it.pos_end = (int32_t)std::min<int64_t>((int64_t)p + e, (lp + 1) * kPage);
+        items.push_back(it);
+      }
+    }
+    n_items = (int64_t)items.size();
+    if (build_blob) {
+      items_bytes.resize(items.size() * sizeof(AppendItem));
+      if (!items.empty()) memcpy(items_bytes.data(), items.data(), items_bytes.size());
+    }
+  } else if (op == TIDE_OP_EXTEND || op == TIDE_OP_FULL_PREFILL) {
+    const int32_t waves = extend_waves(dims.head_dim, group);
+    const int32_t tb = waves * 32 / group;  // tokens per item: waves*32 rows of (token, head)
+    plan->waves = waves;
+    plan->tokens_per_item = tb;
+    struct Costed {
+      int64_t cost;
+      ExtendItem it;
+    };
+    std::vector<Costed> items;
+    for (int32_t b = 0; b < num_tasks; ++b) {
+      const int32_t p = tasks[b].prefix, e = tasks[b].extend;
+      for (int32_t t0 = 0; t0 < e; t0 += tb) {
+        const int32_t n = std::min(tb, e - t0);
+        const int64_t keys = (int64_t)p + t0 + n;
+        for (int32_t g = 0; g < dims.num_kv_heads; ++g) {
+          Costed c;
+          c.cost = keys;
+          c.it.task = b;
+          c.it.kv_head = g;
+          c.it.tok0 = t0;
+          c.it.ntok = n;
+          items.push_back(c);
+        }
+      }
+    }
+    // Longest first, so the short items fill in behind the long ones at the end.
+    std::stable_sort(items.begin(), items.end(),
+                     [](const Costed& x, const Costed& y) { return x.cost > y.cost; });
+    n_items = (int64_t)items.size();
+    if (build_blob) {
+      items_bytes.resize(items.size() * sizeof(ExtendItem));
+      for (size_t i = 0; i < items.size(); ++i)
+        memcpy(items_bytes.data() + i * sizeof(ExtendItem), &items[i].it, sizeof(ExtendItem));
+    }
+  } else {  // decode
+    int64_t chunk = 0;
+    if (num_splits > 0) {
+      for (int32_t b = 0; b < num_tasks; ++b)
+        chunk = std::max<int64_t>(chunk, ceil_div(tasks[b].prefix + 1, num_splits));
+      chunk = std::max<int64_t>(kDecodeStep, ceil_div(chunk, kDecodeStep) * kDecodeStep);
+    } else {
+      int64_t total = 0;
+      for (int32_t b = 0; b < num_tasks; ++b) total += (int64_t)tasks[b].prefix + 1;
+      total *= dims.num_kv_heads;
+      chunk = ceil_div(total, 8192);
+      chunk = ceil_div(chunk, kDecodeStep) * kDecodeStep;
+      chunk = std::min<int64_t>(std::max<int64_t>(chunk, 256), 16384);
+    }
+    int32_t max_splits = 0;
+    std::vector<DecodeItem> items;
+    for (int32_t b = 0; b < num_tasks; ++b) {
+      const int64_t kv = (int64_t)tasks[b].prefix + 1;
+      const int32_t s = (int32_t)ceil_div(kv, chunk);
+      tasks[b].aux = s;
+      max_splits = std::max(max_splits, s);
+      for (int32_t sp = 0; sp < s; ++sp)
+        for (int32_t g = 0; g < dims.num_kv_heads; ++g) {
+          DecodeItem it;
+          it.task = b;
+          it.kv_head = g;
+          it.split = sp;
+          it.k_begin = (int32_t)(sp * chunk);
+          items.push_back(it);
+        }
+    }
+    plan->chunk = (int32_t)chunk;
+    plan->max_splits = max_splits;
+    n_items = (int64_t)items.size();
+    if (build_blob) {
+      items_bytes.resize(items.size() * sizeof(DecodeItem));
+      if (!items.empty()) memcpy(items_bytes.data(), items.data(), items_bytes.size());
+    }
+  }
+  if (n_items > INT32_MAX / 4) return TIDE_ERR_INVALID_ARG;
+  plan->num_items = (int32_t)n_items;
+
+  // ---- layout -------------------------------------------------------------------------
+  size_t off = sizeof(WsHeader);
+  plan->tasks_off = off;
+  off = align_up(off + tasks.size() * sizeof(TaskDesc), kWsAlign);
+  plan->items_off = off;
+  off = align_up(off + (size_t)n_items * 16, kWsAlign);
+  plan->upload_bytes = off;
+  if (op == TIDE_OP_DECODE) {
+    const size_t slots = (size_t)num_tasks * dims.num_q_heads * (size_t)plan->max_splits;
+    plan->part_o_off = off;
+    off = align_up(off + slots * dims.head_dim * sizeof(float), kWsAlign);
+    plan->part_ml_off = off;
+    off = align_up(off + slots * 2 * sizeof(float), kWsAlign);
+  }
+  plan->total_bytes = off;
+
+  if (build_blob) {
+    plan->blob.assign(plan->upload_bytes, 0);
+    if (!tasks.empty())
+      memcpy(plan->blob.data() + plan->tasks_off, tasks.data(), tasks.size() * sizeof(TaskDesc));
+    if (!items_bytes.empty())
+      memcpy(plan->blob.data() + plan->items_off, items_bytes.data(), items_bytes.size());
+  }
+  return TIDE_OK;
+}
+
+}  // namespace tide

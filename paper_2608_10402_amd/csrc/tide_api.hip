@@ -1,0 +1,306 @@
+// The extern "C" entry points declared in include/tide.h: validation and planning on the
+// host (plan.cpp), one host-to-device copy of the work lists into the caller's
+// workspace from a pinned staging ring, then the kernel launches on the caller's stream.
+#include <hip/hip_runtime.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "kernels.h"
+#include "plan.h"
+#include "tide.h"
+
+namespace tide {
+namespace {
+
+constexpr int kStagingSlots = 16;
+constexpr size_t kStagingMin = 64 * 1024;
+
+// Pinned host buffers the work lists are copied from.  A slot is reused only after the
+// event recorded behind its previous copy has completed, so a call never overwrites
+// bytes a queued copy has yet to read.
+struct StagingSlot {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t done = nullptr;
+  bool pending = false;
+};
+
+struct DeviceStaging {
+  StagingSlot slots[kStagingSlots];
+  int next = 0;
+};
+
+std::mutex g_mutex;
+std::vector<DeviceStaging*> g_staging;  // indexed by device ordinal
+
+bool debug_checks() {
+  const char* e = getenv("TIDE_DEBUG_CHECKS");
+  return e && e[0] == '1';
+}
+
+int upload(const Plan& plan, void* workspace, hipStream_t stream) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return TIDE_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_mutex);
+  if ((int)g_staging.size() <= dev) g_staging.resize(dev + 1, nullptr);
+  if (!g_staging[dev]) g_staging[dev] = new DeviceStaging();
+  DeviceStaging& ds = *g_staging[dev];
+  StagingSlot& s = ds.slots[ds.next];
+  ds.next = (ds.next + 1) % kStagingSlots;
+  if (!s.done && hipEventCreateWithFlags(&s.done, hipEventDisableTiming) != hipSuccess)
+    return TIDE_ERR_HIP;
+  if (s.pending) {
+    if (hipEventSynchronize(s.done) != hipSuccess) return TIDE_ERR_HIP;
+    s.pending = false;
+  }
+  const size_t need = plan.blob.size();
+  if (s.cap < need) {
+    if (s.host) (void)hipHostFree(s.host);
+    s.host = nullptr;
+    s.cap = 0;
+    const size_t cap = std::max(kStagingMin, need + need / 4);
+    if (hipHostMalloc(&s.host, cap, hipHostMallocDefault) != hipSuccess) return TIDE_ERR_HIP;
+    s.cap = cap;
+  }
+  memcpy(s.host, plan.blob.data(), need);
+  if (hipMemcpyAsync(workspace, s.host, need, hipMemcpyHostToDevice, stream) != hipSuccess)
+    return TIDE_ERR_HIP;
+  if (hipEventRecord(s.done, stream) != hipSuccess) return TIDE_ERR_HIP;
+  s.pending = true;
+  return TIDE_OK;
+}
+
+int finish(hipError_t launch_status, void* workspace, hipStream_t stream) {
+  if (launch_status != hipSuccess) return TIDE_ERR_HIP;
+  if (!debug_checks()) return TIDE_OK;
+  if (hipStreamSynchronize(stream) != hipSuccess) return TIDE_ERR_HIP;
+  int32_t flags = 0;
+  if (hipMemcpy(&flags, workspace, sizeof(flags), hipMemcpyDeviceToHost) != hipSuccess)
+    return TIDE_ERR_HIP;
+  return (flags & 1) ? TIDE_ERR_PAGE_RANGE : TIDE_OK;
+}
+
+template <class T>
+const T* at(void* ws, size_t off) {
+  return reinterpret_cast<const T*>(static_cast<uint8_t*>(ws) + off);
+}
+
+template <class T>
+T* at_mut(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<uint8_t*>(ws) + off);
+}
+
+// Shared path of tide_extend_attn and tide_full_prefill_attn.
+int run_extend(int op, const void* q, const void* k_pool, const void* v_pool, int64_t num_pages,
+               const int32_t* block_table, int32_t bt_stride, int32_t num_tasks,
+               const int32_t* lens_a, const int32_t* lens_b, const tide_dims* dims, void* out,
+               float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_dims(dims);
+  if (rc != TIDE_OK) return rc;
+  if (num_tasks < 0) return TIDE_ERR_INVALID_ARG;
+  if (num_tasks == 0) return TIDE_OK;
+  if (num_pages <= 0 || bt_stride <= 0) return TIDE_ERR_INVALID_ARG;
+  Plan plan;
+  rc = make_plan(op, num_tasks, lens_a, lens_b, *dims, 0, bt_stride, true, &plan);
+  if (rc != TIDE_OK) return rc;
+  if (plan.num_items == 0) return TIDE_OK;
+  if (!q || !k_pool || !v_pool || !block_table || !out || !workspace) return TIDE_ERR_INVALID_ARG;
+  if (workspace_bytes < plan.total_bytes) return TIDE_ERR_CAPACITY;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  rc = upload(plan, workspace, s);
+  if (rc != TIDE_OK) return rc;
+  ExtendArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.block_table = block_table;
+  a.num_pages = num_pages;
+  a.bt_stride = bt_stride;
+  a.num_q_heads = dims->num_q_heads;
+  a.num_kv_heads = dims->num_kv_heads;
+  a.group = dims->num_q_heads / dims->num_kv_heads;
+  a.scale_log2 = dims->sm_scale * 1.44269504088896340736f;
+  a.num_items = plan.num_items;
+  a.tasks = at<TaskDesc>(workspace, plan.tasks_off);
+  a.items = at<ExtendItem>(workspace, plan.items_off);
+  a.out = static_cast<uint16_t*>(out);
+  a.lse = lse;
+  a.error_flags = at_mut<int32_t>(workspace, 0);
+  return finish(launch_extend(a, dims->head_dim, plan.waves, s), workspace, s);
+}
+
+}  // namespace
+}  // namespace tide
+
+using namespace tide;
+
+extern "C" {
+
+TIDE_API int tide_workspace_size(int op, int32_t num_tasks, const int32_t* lens_a,
+                                 const int32_t* lens_b, const tide_dims* dims,
+                                 int32_t num_splits, size_t* bytes_out) {
+  try {
+    if (!bytes_out) return TIDE_ERR_INVALID_ARG;
+    int rc = check_dims(dims);
+    if (rc != TIDE_OK) return rc;
+    Plan plan;
+    rc = make_plan(op, num_tasks, lens_a, lens_b, *dims, num_splits, -1, false, &plan);
+    if (rc != TIDE_OK) return rc;
+    *bytes_out = plan.total_bytes;
+    return TIDE_OK;
+  } catch (...) {
+    return TIDE_ERR_HIP;
+  }
+}
+
+TIDE_API int tide_kv_append(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                            int64_t num_pages, const int32_t* block_table, int32_t bt_stride,
+                            int32_t num_tasks, const int32_t* prefix_lens,
+                            const int32_t* extend_lens, const tide_dims* dims, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  try {
+    int rc = check_dims(dims);
+    if (rc != TIDE_OK) return rc;
+    if (num_tasks < 0) return TIDE_ERR_INVALID_ARG;
+    if (num_tasks == 0) return TIDE_OK;
+    if (num_pages <= 0 || bt_stride <= 0) return TIDE_ERR_INVALID_ARG;
+    Plan plan;
+    rc = make_plan(TIDE_OP_KV_APPEND, num_tasks, prefix_lens, extend_lens, *dims, 0, bt_stride,
+                   true, &plan);
+    if (rc != TIDE_OK) return rc;
+    if (plan.num_items == 0) return TIDE_OK;
+    if (!k_new || !v_new || !k_pool || !v_pool || !block_table || !workspace)
+      return TIDE_ERR_INVALID_ARG;
+    if (workspace_bytes < plan.total_bytes) return TIDE_ERR_CAPACITY;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    rc = upload(plan, workspace, s);
+    if (rc != TIDE_OK) return rc;
+    AppendArgs a;
+    a.k_new = static_cast<const uint16_t*>(k_new);
+    a.v_new = static_cast<const uint16_t*>(v_new);
+    a.k_pool = static_cast<uint16_t*>(k_pool);
+    a.v_pool = static_cast<uint16_t*>(v_pool);
+    a.block_table = block_table;
+    a.num_pages = num_pages;
+    a.bt_stride = bt_stride;
+    a.num_kv_heads = dims->num_kv_heads;
+    a.head_dim = dims->head_dim;
+    a.num_items = plan.num_items;
+    a.tasks = at<TaskDesc>(workspace, plan.tasks_off);
+    a.items = at<AppendItem>(workspace, plan.items_off);
+    a.error_flags = at_mut<int32_t>(workspace, 0);
+    return finish(launch_kv_append(a, s), workspace, s);
+  } catch (...) {
+    return TIDE_ERR_HIP;
+  }
+}
+
+TIDE_API int tide_extend_attn(const void* q, const void* k_pool, const void* v_pool,
+                              int64_t num_pages, const int32_t* block_table, int32_t bt_stride,
+                              int32_t num_tasks, const int32_t* prefix_lens,
+                              const int32_t* extend_lens, const tide_dims* dims, void* out,
+                              float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    return run_extend(TIDE_OP_EXTEND, q, k_pool, v_pool, num_pages, block_table, bt_stride,
+                      num_tasks, prefix_lens, extend_lens, dims, out, lse, workspace,
+                      workspace_bytes, stream);
+  } catch (...) {
+    return TIDE_ERR_HIP;
+  }
+}
+
+TIDE_API int tide_full_prefill_attn(const void* q, const void* k_pool, const void* v_pool,
+                                    int64_t num_pages, const int32_t* block_table,
+                                    int32_t bt_stride, int32_t num_tasks, const int32_t* seq_lens,
+                                    const tide_dims* dims, void* out, float* lse,
+                                    void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    return run_extend(TIDE_OP_FULL_PREFILL, q, k_pool, v_pool, num_pages, block_table,
+                      bt_stride, num_tasks, seq_lens, nullptr, dims, out, lse, workspace,
+                      workspace_bytes, stream);
+  } catch (...) {
+    return TIDE_ERR_HIP;
+  }
+}
+
+TIDE_API int tide_decode_attn(const void* q, const void* k_pool, const void* v_pool,
+                              int64_t num_pages, const int32_t* block_table, int32_t bt_stride,
+                              int32_t num_tasks, const int32_t* kv_lens, const tide_dims* dims,
+                              int32_t num_splits, void* out, float* lse, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  try {
+    int rc = check_dims(dims);
+    if (rc != TIDE_OK) return rc;
+    if (num_tasks < 0 || num_splits < 0) return TIDE_ERR_INVALID_ARG;
+    if (num_tasks == 0) return TIDE_OK;
+    if (num_pages <= 0 || bt_stride <= 0) return TIDE_ERR_INVALID_ARG;
+    Plan plan;
+    rc = make_plan(TIDE_OP_DECODE, num_tasks, kv_lens, nullptr, *dims, num_splits, bt_stride,
+                   true, &plan);
+    if (rc != TIDE_OK) return rc;
+    if (!q || !k_pool || !v_pool || !block_table || !out || !workspace)
+      return TIDE_ERR_INVALID_ARG;
+    if (workspace_bytes < plan.total_bytes) return TIDE_ERR_CAPACITY;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    rc = upload(plan, workspace, s);
+    if (rc != TIDE_OK) return rc;
+    DecodeArgs a;
+    a.q = static_cast<const uint16_t*>(q);
+    a.k_pool = static_cast<const uint16_t*>(k_pool);
+    a.v_pool = static_cast<const uint16_t*>(v_pool);
+    a.block_table = block_table;
+    a.num_pages = num_pages;
+    a.bt_stride = bt_stride;
+    a.num_q_heads = dims->num_q_heads;
+    a.num_kv_heads = dims->num_kv_heads;
+    a.group = dims->num_q_heads / dims->num_kv_heads;
+    a.scale_log2 = dims->sm_scale * 1.44269504088896340736f;
+    a.num_tasks = num_tasks;
+    a.num_items = plan.num_items;
+    a.chunk = plan.chunk;
+    a.max_splits = plan.max_splits;
+    a.tasks = at<TaskDesc>(workspace, plan.tasks_off);
+    a.items = at<DecodeItem>(workspace, plan.items_off);
+    a.part_o = at_mut<float>(workspace, plan.part_o_off);
+    a.part_ml = at_mut<float>(workspace, plan.part_ml_off);
+    a.out = static_cast<uint16_t*>(out);
+    a.lse = lse;
+    a.error_flags = at_mut<int32_t>(workspace, 0);
+    return finish(launch_decode(a, dims->head_dim, s), workspace, s);
+  } catch (...) {
+    return TIDE_ERR_HIP;
+  }
+}
+
+TIDE_API const char* tide_status_string(int status) {
+  switch (status) {
+    case TIDE_OK: return "ok";
+    case TIDE_ERR_INVALID_ARG: return "invalid argument";
+    case TIDE_ERR_UNSUPPORTED: return "unsupported shape";
+    case TIDE_ERR_CAPACITY: return "capacity exceeded (block table or workspace too small)";
+    case TIDE_ERR_HIP: return "HIP runtime error";
+    case TIDE_ERR_PAGE_RANGE: return "block-table page id out of range";
+    default: return "unknown status";
+  }
+}
+
+TIDE_API void tide_shutdown(void) {
+  std::lock_guard<std::mutex> lock(g_mutex);
+  for (DeviceStaging* ds : g_staging) {
+    if (!ds) continue;
+    for (StagingSlot& s : ds->slots) {
+      if (s.pending && s.done) (void)hipEventSynchronize(s.done);
+      if (s.done) (void)hipEventDestroy(s.done);
+      if (s.host) (void)hipHostFree(s.host);
+    }
+    delete ds;
+  }
+  g_staging.clear();
+}
+
+}  // extern "C"

@@ -1,0 +1,115 @@
+// Definitions shared by the host planner and the gfx950 kernels: the work-item records
+// uploaded into the caller's workspace, and the kernel argument blocks.
+#pragma once
+
+#include <stdint.h>
+
+namespace tide {
+
+constexpr int kPage = 16;         // tokens per page
+constexpr int kMaxGroup = 16;     // largest supported Hq / Hkv
+constexpr int kExtendKeyTile = 64;  // keys per extend-kernel iteration (4 pages)
+constexpr int kDecodeStep = 32;   // keys per decode-kernel iteration (2 pages)
+constexpr int kWsAlign = 256;
+
+// One task as the kernels see it.  `row_start` indexes the packed token rows of Q/O
+// (extend, prefill) or the task itself (decode); tokens at positions
+// [prefix, prefix + extend) are the ones this call processes.
+struct TaskDesc {
+  int32_t row_start;
+  int32_t prefix;
+  int32_t extend;
+  int32_t aux;  // decode: number of splits of this task; append: first new-row index
+};
+
+// Extend / prefill work item: tokens [tok0, tok0 + ntok) of `task` (relative to its
+// prefix) for every query head that reads kv head `kv_head`.
+struct ExtendItem {
+  int32_t task;
+  int32_t kv_head;
+  int32_t tok0;
+  int32_t ntok;
+};
+
+// Decode split-K item: keys [k_begin, min(kv_len, k_begin + chunk)) of one (task, kv head).
+struct DecodeItem {
+  int32_t task;
+  int32_t kv_head;
+  int32_t split;
+  int32_t k_begin;
+};
+
+// Append item: positions [pos_begin, pos_end) of `task`, all inside logical page `lpage`.
+struct AppendItem {
+  int32_t task;
+  int32_t lpage;
+  int32_t pos_begin;
+  int32_t pos_end;
+};
+
+// Layout of the per-call header at the start of the workspace.
+struct WsHeader {
+  int32_t error_flags;  // bit 0: a block-table page id was outside [0, num_pages)
+  int32_t pad[63];
+};
+
+struct AppendArgs {
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  uint16_t* k_pool;
+  uint16_t* v_pool;
+  const int32_t* block_table;
+  int64_t num_pages;
+  int32_t bt_stride;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t num_items;
+  const TaskDesc* tasks;
+  const AppendItem* items;
+  int32_t* error_flags;
+};
+
+struct ExtendArgs {
+  const uint16_t* q;
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* block_table;
+  int64_t num_pages;
+  int32_t bt_stride;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t group;
+  float scale_log2;  // sm_scale * log2(e): scores are kept in base-2 units
+  int32_t num_items;
+  const TaskDesc* tasks;
+  const ExtendItem* items;
+  uint16_t* out;
+  float* lse;
+  int32_t* error_flags;
+};
+
+struct DecodeArgs {
+  const uint16_t* q;
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* block_table;
+  int64_t num_pages;
+  int32_t bt_stride;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t group;
+  float scale_log2;
+  int32_t num_tasks;
+  int32_t num_items;
+  int32_t chunk;       // keys per split (multiple of kDecodeStep)
+  int32_t max_splits;  // split slots per (task, q head) in the partial buffers
+  const TaskDesc* tasks;  // prefix + extend == kv_len, aux == number of splits
+  const DecodeItem* items;
+  float* part_o;   // [num_tasks][Hq][max_splits][d] unnormalised partial outputs
+  float* part_ml;  // [num_tasks][Hq][max_splits][2] (running max in base-2 units, sum)
+  uint16_t* out;
+  float* lse;
+  int32_t* error_flags;
+};
+
+}  // namespace tide

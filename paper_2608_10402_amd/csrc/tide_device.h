@@ -1,0 +1,79 @@
+// Device helpers for the gfx950 kernels: vector types, bf16 packing, MFMA wrappers and
+// the lane-permutation that makes MFMA outputs feed the next MFMA directly.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tide_common.h"
+
+namespace tide {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLn2 = 0.69314718055994530942f;
+constexpr float kLog2e = 1.44269504088896340736f;
+// Running-max sentinel: finite so that exp2(m_old - m_new) never sees (-inf) - (-inf).
+constexpr float kNoMax = -1.0e30f;
+// A row's reference max is only raised when the tile max exceeds it by more than this
+// (base-2 units).  Unnormalised weights then stay <= 2^8, far from fp32/bf16 limits,
+// and the accumulator rescale is skipped on almost every tile.
+constexpr float kRescaleSlack = 8.0f;
+
+__device__ __forceinline__ u32x4 load_u32x4(const void* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+
+__device__ __forceinline__ void store_u32x4(void* p, u32x4 v) {
+  *reinterpret_cast<u32x4*>(p) = v;
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ u32x4 zero_u32x4() {
+  u32x4 z = {0u, 0u, 0u, 0u};
+  return z;
+}
+
+// Two fp32 values -> packed bf16 pair (round to nearest even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ float xor_shfl(float v, int mask) {
+  return __shfl_xor(v, mask, 64);
+}
+
+// v_mfma_f32_32x32x16_bf16.  Lane layouts (checked on gfx950):
+//   A: lane l holds row l%32, k = 8*(l/32) .. +7;  B: lane l holds column l%32, same k;
+//   D: lane l register r holds row 8*(r/4) + 4*(l/32) + r%4, column l%32.
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// v_mfma_f32_16x16x32_bf16.  A: lane l row l%16, k = 8*(l/16) .. +7; B: column l%16;
+//   D: lane l register r holds row 4*(l/16) + r, column l%16.
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Row permutation for the 32x32 tiles.  When the 32 rows of an S^T = K.Q^T tile are the
+// keys kappa(0..31), the D registers r = 0..7 of lane l hold keys 8*(l/32) + r and
+// registers 8..15 hold 16 + 8*(l/32) + (r - 8): each lane owns runs of 8 consecutive
+// keys, which is exactly the B operand of the P.V product over 16 keys.  The same
+// permutation applied to the rows of V^T makes each lane's outputs 8 consecutive
+// head-dim entries, so results leave in 16-byte stores.
+__device__ __forceinline__ int perm32(int rho) {
+  const int j = rho >> 3, h = (rho >> 2) & 1, r = rho & 3;
+  return 16 * (j >> 1) + 8 * h + 4 * (j & 1) + r;
+}
+
+}  // namespace tide

@@ -1,0 +1,97 @@
+"""Test-side glue: put a seeded workload on the GPU through the library's own calls,
+and compare results with the oracle.
+
+The GPU pool is filled only by tide_kv_append (first the retained prefix, then the new
+tokens), the oracle pool only by the oracle's own append; the two never exchange data.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+import oracle_pins
+import paper_2608_10402_amd as tide
+import workloads as W
+
+MAX_ABS_TOL = 2e-2   # bf16 outputs vs fp64 oracle: max |error|
+MEAN_ABS_TOL = 2e-3  # and mean |error|
+LSE_TOL = 1e-3
+
+
+def log(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def dev_bf16(bits: np.ndarray, device="cuda") -> torch.Tensor:
+    bits = np.ascontiguousarray(bits, dtype=np.uint16)
+    return torch.from_numpy(bits.view(np.int16)).to(device).view(torch.bfloat16)
+
+
+def host_bits(t: torch.Tensor) -> np.ndarray:
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def host_f64(t: torch.Tensor) -> np.ndarray:
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+class DeviceWorkload:
+    """Device pools of a workload, with the prefix already appended."""
+
+    def __init__(self, wl: W.Workload, device="cuda"):
+        self.wl = wl
+        s = wl.spec
+        self.kv = tide.PagedKV(wl.num_pages, s.num_q_heads, s.num_kv_heads, s.head_dim,
+                               wl.block_table, wl.sm_scale, device=device)
+        zeros = np.zeros(wl.num_tasks, np.int32)
+        if wl.prefix_lens.sum() > 0:
+            self.kv.append(dev_bf16(wl.packed("k", wl.prefix_ranges())),
+                           dev_bf16(wl.packed("v", wl.prefix_ranges())), zeros, wl.prefix_lens)
+
+    def append_extend(self):
+        wl = self.wl
+        self.kv.append(dev_bf16(wl.packed("k", wl.extend_ranges())),
+                       dev_bf16(wl.packed("v", wl.extend_ranges())), wl.prefix_lens,
+                       wl.extend_lens)
+
+    def extend(self, lse=True):
+        wl = self.wl
+        q = dev_bf16(wl.packed("q", wl.extend_ranges()))
+        l = torch.empty((q.shape[0], q.shape[1]), dtype=torch.float32, device=q.device) if lse else None
+        out = self.kv.extend(q, wl.prefix_lens, wl.extend_lens, lse=l)
+        return out, l
+
+    def prefill(self, lse=True):
+        wl = self.wl
+        q = dev_bf16(wl.packed("q", wl.full_ranges()))
+        l = torch.empty((q.shape[0], q.shape[1]), dtype=torch.float32, device=q.device) if lse else None
+        out = self.kv.prefill(q, wl.seq_lens, lse=l)
+        return out, l
+
+
+def oracle_pools(wl: W.Workload):
+    return oracle_pins.oracle_pools_for(wl)
+
+
+def assert_close(gpu: torch.Tensor, ref: np.ndarray, what: str, max_tol=MAX_ABS_TOL,
+                 mean_tol=MEAN_ABS_TOL):
+    g = host_f64(gpu)
+    assert g.shape == ref.shape, (what, g.shape, ref.shape)
+    assert np.isfinite(g).all(), "%s: non-finite GPU output" % what
+    err = np.abs(g - ref)
+    mx, mean = float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
+    log("%s: max abs err %.3e, mean abs err %.3e over %d values" % (what, mx, mean, err.size))
+    assert mx <= max_tol, "%s: max abs error %.4g > %.4g" % (what, mx, max_tol)
+    assert mean <= mean_tol, "%s: mean abs error %.4g > %.4g" % (what, mean, mean_tol)
+
+
+def assert_lse(gpu: torch.Tensor, ref: np.ndarray, what: str, tol=LSE_TOL):
+    g = gpu.cpu().numpy().astype(np.float64)
+    err = np.abs(g - ref)
+    mx = float(err.max()) if err.size else 0.0
+    log("%s: lse max abs err %.3e" % (what, mx))
+    assert mx <= tol, "%s: lse error %.4g > %.4g" % (what, mx, tol)
