@@ -1,0 +1,296 @@
+#!/usr/bin/env python3
+"""Benchmark of the paged-KV resume-attention hot path on one MI355X.
+
+One step is one pass over every stage of the path for the agent-resume workload
+(64 tasks, 28 query / 4 KV heads, head_dim 128, page 16, prefixes U{2048..16384},
+observations log-uniform 64..2048, fragmented page placement):
+    1. KV-append of the new observation tokens           (tide_kv_append)
+    2. extend attention over the retained prefix         (tide_extend_attn)
+    3. decode attention of one token per task (split-K)  (tide_decode_attn)
+    4. the recompute a cache miss forces: KV-append of the whole history, then
+       full causal re-prefill attention                   (tide_kv_append, tide_full_prefill_attn)
+Inputs are resident in HBM before timing starts; every kernel call is timed with HIP
+events on the stream it is launched on.
+
+Printed: one JSON line.  `value` is extend-attention throughput in TFLOP/s over the
+unmasked (query, key) pairs (4*d flops per pair and query head).  The line also
+carries the decode GB/s, the speedup of extend over re-prefill, the roofline of the
+dominant kernel, and the fp64 oracle timed on a bounded sample on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "extend-attn TFLOP/s (% bf16 peak); decode-attn GB/s (% HBM); speedup vs re-prefill"
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+PROFILE_SUMMARY = os.path.join(ROOT, "profiles", "attn_extend_agent_resume_7b_counters.txt")
+EXTEND_SOURCE = os.path.join(ROOT, "paper_2608_10402_amd", "csrc", "attn_extend.hip")
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="agent_resume_7b")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="wall-time budget of the oracle CPU baseline sample (0 disables it)")
+    ap.add_argument("--skip-reprefill", action="store_true",
+                    help="leave out stage 4 (for profiling the other kernels only)")
+    return ap.parse_args()
+
+
+def extend_flops(wl) -> float:
+    p = wl.prefix_lens.astype(np.float64)
+    e = wl.extend_lens.astype(np.float64)
+    pairs = float(np.sum(e * p + e * (e + 1) / 2))
+    return 4.0 * wl.spec.head_dim * wl.spec.num_q_heads * pairs
+
+
+def prefill_flops(wl) -> float:
+    l = wl.seq_lens.astype(np.float64)
+    return 4.0 * wl.spec.head_dim * wl.spec.num_q_heads * float(np.sum(l * (l + 1) / 2))
+
+
+def decode_bytes(wl, kv_lens) -> float:
+    s = wl.spec
+    kv = float(np.sum(kv_lens)) * s.num_kv_heads * s.head_dim * 2 * 2  # K and V once
+    qo = wl.num_tasks * s.num_q_heads * s.head_dim * 2 * 2              # Q in, O out
+    bt = float(np.sum(-(-np.asarray(kv_lens) // 16))) * 4                 # page ids read
+    return kv + qo + bt
+
+
+def append_bytes(wl, tokens: int) -> float:
+    s = wl.spec
+    return float(tokens) * s.num_kv_heads * s.head_dim * 2 * 2 * 2  # K+V, read + write
+
+
+def counter_traffic():
+    """HBM bytes per extend launch from the committed rocprofv3 counter summary, or None
+    when the kernel source changed since the counters were taken."""
+    if not os.path.exists(PROFILE_SUMMARY):
+        return None
+    text = open(PROFILE_SUMMARY).read()
+    m_hash = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
+    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes:
+        return None
+    cur = hashlib.sha256(open(EXTEND_SOURCE, "rb").read()).hexdigest()
+    return float(m_bytes.group(1)) if cur == m_hash.group(1) else None
+
+
+def cpu_baseline(wl, q_ext_host, budget_s: float):
+    """The fp64 oracle on a bounded, seeded sample of extend rows (host cores)."""
+    import oracle
+    s = wl.spec
+    kp, vp = oracle.new_pools(wl.num_pages, s.num_kv_heads, s.head_dim)
+    zeros = np.zeros(wl.num_tasks, np.int32)
+    oracle.kv_append(wl.packed("k", wl.prefix_ranges()), wl.packed("v", wl.prefix_ranges()),
+                     kp, vp, wl.block_table, zeros, wl.prefix_lens)
+    oracle.kv_append(wl.packed("k", wl.extend_ranges()), wl.packed("v", wl.extend_ranges()),
+                     kp, vp, wl.block_table, wl.prefix_lens, wl.extend_lens)
+    indptr = np.concatenate([[0], np.cumsum(wl.extend_lens)]).astype(np.int64)
+    rng = np.random.default_rng(2608)
+    rows = []
+    for b in range(wl.num_tasks):
+        e = int(wl.extend_lens[b])
+        if e:
+            rows += [indptr[b], indptr[b] + e - 1]
+    rows += rng.integers(0, int(indptr[-1]), size=4096).tolist()
+    rows = np.array(list(dict.fromkeys(int(r) for r in rows)), dtype=np.int64)
+    rng.shuffle(rows)
+    threads = oracle.threads()
+    done, flops, t0 = 0, 0.0, time.time()
+    outs = []
+    while done < rows.size and time.time() - t0 < budget_s:
+        batch = rows[done:done + 4 * threads]
+        o, _ = oracle.attention(q_ext_host[batch], batch, kp, vp, wl.block_table, wl.prefix_lens,
+                                wl.extend_lens, s.num_q_heads, wl.sm_scale, nthreads=threads)
+        task = np.searchsorted(indptr, batch, side="right") - 1
+        pos = wl.prefix_lens[task] + (batch - indptr[task])
+        flops += 4.0 * s.head_dim * s.num_q_heads * float(np.sum(pos + 1))
+        outs.append((batch, o))
+        done += batch.size
+    dt = time.time() - t0
+    info = {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": "%d of %d extend rows (every task's first and last row, then seeded "
+                      "random rows), all %d query heads, fp64, %.1f s wall"
+                      % (done, int(indptr[-1]), s.num_q_heads, dt),
+            "seconds": round(dt, 2), "flops": flops}
+    return info, outs
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this library has no multi-GPU path (each GPU would "
+              "run its own rank's tasks independently). Run with --gpus 1.", file=sys.stderr)
+        return 2
+    import torch
+    import paper_2608_10402_amd as tide
+    import workloads as W
+
+    tide.load()  # fail loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    wl = W.make_workload(args.workload)
+    s = wl.spec
+    assert s.kind == "extend", "the benchmark step needs an extend workload"
+
+    def up(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    t_setup = time.time()
+    k_pre = up(wl.packed("k", wl.prefix_ranges()))
+    v_pre = up(wl.packed("v", wl.prefix_ranges()))
+    k_ext = up(wl.packed("k", wl.extend_ranges()))
+    v_ext = up(wl.packed("v", wl.extend_ranges()))
+    q_ext_host = wl.packed("q", wl.extend_ranges())
+    q_ext = up(q_ext_host)
+    k_full = up(wl.packed("k", wl.full_ranges()))
+    v_full = up(wl.packed("v", wl.full_ranges()))
+    q_full = None if args.skip_reprefill else up(wl.packed("q", wl.full_ranges()))
+    kv = tide.PagedKV(wl.num_pages, s.num_q_heads, s.num_kv_heads, s.head_dim, wl.block_table,
+                      wl.sm_scale, device=dev)
+    zeros = np.zeros(wl.num_tasks, np.int32)
+    kv.append(k_pre, v_pre, zeros, wl.prefix_lens)
+    # decode: the last resumed token of each task as the query over its whole context
+    last_rows = np.cumsum(wl.extend_lens) - 1
+    q_dec = q_ext[torch.from_numpy(last_rows.astype(np.int64)).to(dev)].contiguous()
+    out_ext = torch.empty_like(q_ext)
+    out_dec = torch.empty_like(q_dec)
+    out_full = None if q_full is None else torch.empty_like(q_full)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t_setup
+
+    stream = torch.cuda.current_stream()
+    stages = ["append_new", "extend", "decode"] + ([] if q_full is None else
+                                                   ["append_history", "prefill"])
+    ev = {k: [] for k in stages}
+
+    def step(record):
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] if record else None
+        if record:
+            marks[0].record(stream)
+        kv.append(k_ext, v_ext, wl.prefix_lens, wl.extend_lens)
+        if record:
+            marks[1].record(stream)
+        kv.extend(q_ext, wl.prefix_lens, wl.extend_lens, out=out_ext)
+        if record:
+            marks[2].record(stream)
+        kv.decode(q_dec, wl.seq_lens, out=out_dec)
+        if record:
+            marks[3].record(stream)
+        if q_full is not None:
+            kv.append(k_full, v_full, zeros, wl.seq_lens)
+            if record:
+                marks[4].record(stream)
+            kv.prefill(q_full, wl.seq_lens, out=out_full)
+            if record:
+                marks[5].record(stream)
+        if record:
+            for i, k in enumerate(stages):
+                ev[k].append((marks[i], marks[i + 1]))
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = {k: float(np.mean([a.elapsed_time(b) for a, b in v])) for k, v in ev.items()}
+
+    f_ext = extend_flops(wl)
+    ext_tflops = f_ext / (ms["extend"] * 1e-3) / 1e12
+    dec_bytes = decode_bytes(wl, wl.seq_lens)
+    dec_gbs = dec_bytes / (ms["decode"] * 1e-3) / 1e9
+    app_gbs = append_bytes(wl, int(wl.extend_lens.sum())) / (ms["append_new"] * 1e-3) / 1e9
+    extra = {
+        "stage_ms": {k: round(v, 4) for k, v in ms.items()},
+        "extend_tflops": round(ext_tflops, 2),
+        "extend_bf16_peak_frac": round(ext_tflops / PEAK_BF16_TFLOPS, 4),
+        "extend_tokens_per_s": round(float(wl.extend_lens.sum()) / (ms["extend"] * 1e-3), 1),
+        "decode_gbs": round(dec_gbs, 1),
+        "decode_hbm_frac": round(dec_gbs / PEAK_HBM_GBS, 4),
+        "decode_note": "one query per task (its last resumed token) over the whole context",
+        "append_gbs": round(app_gbs, 1),
+        "setup_s": round(setup_s, 1),
+    }
+    rooflines = {
+        "extend": {"bound": "mfma", "achieved": round(ext_tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                   "unit": "TFLOP/s", "frac": round(ext_tflops / PEAK_BF16_TFLOPS, 4)},
+        "decode": {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": PEAK_HBM_GBS,
+                   "unit": "GB/s", "frac": round(dec_gbs / PEAK_HBM_GBS, 4)},
+    }
+    if q_full is not None:
+        f_pre = prefill_flops(wl)
+        pre_tflops = f_pre / (ms["prefill"] * 1e-3) / 1e12
+        resume = ms["append_new"] + ms["extend"]
+        recompute = ms["append_history"] + ms["prefill"]
+        extra.update({
+            "prefill_tflops": round(pre_tflops, 2),
+            "prefill_bf16_peak_frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4),
+            "speedup_vs_reprefill": round(recompute / resume, 3),
+            "speedup_vs_reprefill_attention_only": round(ms["prefill"] / ms["extend"], 3),
+            "flop_ratio_prefill_over_extend": round(f_pre / f_ext, 3),
+        })
+        rooflines["prefill"] = {"bound": "mfma", "achieved": round(pre_tflops, 2),
+                                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                                "frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4)}
+    roofline = dict(rooflines["extend"])
+    roofline["traffic"] = counter_traffic()
+    roofline["kernel"] = "extend_attn_kernel"
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu, outs = cpu_baseline(wl, q_ext_host, args.cpu_seconds)
+        got = out_ext.float().cpu().numpy()
+        errs = [np.abs(got[b] - o) for b, o in outs]
+        if errs:
+            e = np.concatenate([x.ravel() for x in errs])
+            extra["parity_sampled_rows"] = {"rows": int(sum(len(b) for b, _ in outs)),
+                                            "max_abs_err": float(e.max()),
+                                            "mean_abs_err": float(e.mean())}
+
+    line = {
+        "metric": METRIC,
+        "value": round(ext_tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.spec.key, "tasks": wl.num_tasks, "q_heads": s.num_q_heads,
+                   "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "page_size": s.page_size,
+                   "extend_tokens": int(wl.extend_lens.sum()), "context_tokens": int(wl.seq_lens.sum()),
+                   "pool_pages": wl.num_pages, "lens_digest": wl.lens_digest()},
+        "roofline": roofline,
+        "rooflines": rooflines,
+        "cpu_baseline": cpu,
+        "extra": extra,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

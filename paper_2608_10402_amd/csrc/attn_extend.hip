@@ -6,141 +6,154 @@
 // Method: FlashAttention-2-style streaming softmax (Dao 2023; online softmax of Milakov
 // & Gimelshein 2018) over K/V gathered page by page (PagedAttention, Kwon et al. 2023),
 // laid out for CDNA4:
-//   * A workgroup owns one (task, kv head, block of tokens) item.  Its NW*32 query rows
-//     are the (token, head) pairs of the block for every query head of the kv head, so
-//     each K/V tile staged in LDS serves all G grouped heads at once.
+//   * A workgroup (4 waves) owns one (task, kv head, block of tokens) item.  Its 128
+//     query rows are the (token, head) pairs of the block for every query head of the kv
+//     head, so each K/V tile in LDS serves all G grouped heads at once.
+//   * K/V tiles of 64 keys (4 pages) go from HBM straight into LDS with
+//     global_load_lds_dwordx4 (no staging registers); wave w fetches page w of the tile.
+//     Two LDS buffers: the next tile streams in while the current one is used.
 //   * Each wave computes S^T = K.Q^T for its 32 rows with v_mfma_f32_32x32x16_bf16:
 //     keys are the MFMA rows, queries the columns, so every lane owns one query row and
-//     its softmax statistics need only one cross-lane exchange (lanes l and l^32).
-//   * Key rows are loaded in the perm32 order, which leaves each lane holding runs of 8
+//     its softmax statistics need one cross-lane exchange (lanes l and l^32).
+//   * Key rows are read in the perm32 order, which leaves each lane holding runs of 8
 //     consecutive keys: the probabilities convert straight into the B operand of the
-//     O^T += V^T.P^T MFMA without any shuffle.  V pages are stored transposed in the
-//     pool (head-dim major, 16 token slots contiguous), so V^T operands are plain
-//     16-byte LDS reads.
-//   * Scores are kept in base-2 units (sm_scale * log2 e folded in) and exponentiated
-//     with v_exp_f32.  The running max is only raised when a tile exceeds it by more
-//     than kRescaleSlack, so the O rescale is skipped on almost every tile.
-//   * Causal masking is applied only on the tiles that cross the diagonal, and V slots
-//     at or beyond the task's length are zeroed while staging so that NaN/Inf garbage in
-//     unused pool slots can never reach the output.
+//     O^T += V^T.P^T MFMA with no shuffle.  V pages are stored transposed in the pool
+//     (head-dim major, 16 token slots contiguous), so V^T operands are plain 16-byte LDS
+//     reads.  K rows are XOR-swizzled by 16-byte granule in LDS so that the 64 lanes of an
+//     operand read hit distinct banks.
+//   * Scores stay raw until one FMA applies sm_scale*log2(e) and subtracts the running
+//     max before v_exp_f32.  The running max is only raised when a tile exceeds it by
+//     more than kRescaleSlack, so the O rescale is skipped on almost every tile.
+//   * Causal masking is applied only on tiles that cross the diagonal.  V slots at or
+//     beyond the task's length (the last tile) are zeroed in LDS before use, so NaN/Inf
+//     garbage in unused pool slots can never reach the output.
+//   * At most 256 registers per lane, so two workgroups share a CU and one's softmax
+//     overlaps the other's matrix work.
 #include "kernels.h"
 #include "tide_device.h"
 
 namespace tide {
 namespace {
 
-template <int D, int NW>
-struct Shape {
-  static constexpr int kThreads = NW * 64;
-  static constexpr int kKeys = kExtendKeyTile;          // 64 keys = 4 pages per tile
-  static constexpr int kPages = kKeys / kPage;
-  static constexpr int kKPitch = D + 8;                 // padded K row (bf16 elements)
-  static constexpr int kKTile = kKeys * kKPitch;
-  static constexpr int kVTile = kPages * D * kPage;     // 4 transposed pages
-  static constexpr int kKChunks = kKeys * D / 8;        // 16-byte chunks per tile
-  static constexpr int kVChunks = kVTile / 8;
-  static constexpr int kKPer = kKChunks / kThreads;
-  static constexpr int kVPer = kVChunks / kThreads;
-  static_assert(kKChunks % kThreads == 0 && kVChunks % kThreads == 0, "tile split");
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * 64;
+
+template <int D>
+struct ES {
+  static constexpr int kNG = D / 8;             // 16-byte granules per K row
+  static constexpr int kRB = 16 / kNG;          // K rows per 256-byte LDS bank row
+  static constexpr int kRowBytes = D * 2;
+  static constexpr int kPageBytes = kPage * kRowBytes;
+  static constexpr int kTileBytes = 4 * kPageBytes;  // 64 keys
+  static constexpr int kDma = kPageBytes / 1024;     // 1 KB wave transfers per page
+  static constexpr int kRowsPerDma = 1024 / kRowBytes;
+  static_assert(kDma >= 1 && kRowsPerDma * kRowBytes == 1024, "page split");
 };
 
-template <int D, int NW>
-struct Staged {
-  u32x4 k[Shape<D, NW>::kKPer];
-  u32x4 v[Shape<D, NW>::kVPer];
+// Swizzled position of granule g in K row r.
+template <int D>
+__device__ __forceinline__ int kswz(int r, int g) {
+  return g ^ ((r / ES<D>::kRB) % ES<D>::kNG);
+}
+
+__device__ __forceinline__ void wait_all_vmem() {
+  // s_waitcnt vmcnt(0) (gfx9 encoding: expcnt and lgkmcnt left at their maxima)
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+}
+
+template <int D>
+struct Ctx {
+  const ExtendArgs* a;
+  const int32_t* bt_row;
+  int npages;
+  int seq_len;
+  int kv_head;
+  int wave;
+  int lane;
+  int k_dma_off[ES<D>::kDma];  // this lane's source offset inside a K page, per transfer
 };
 
-// Keep only the first n (0..8) bf16 elements of a 16-byte chunk.
-__device__ __forceinline__ u32x4 keep_first(u32x4 x, int n) {
-  u32x4 r;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    const uint32_t lo = (2 * w < n) ? 0x0000FFFFu : 0u;
-    const uint32_t hi = (2 * w + 1 < n) ? 0xFFFF0000u : 0u;
-    r[w] = x[w] & (lo | hi);
-  }
-  return r;
-}
-
-template <int D, int NW>
-__device__ __forceinline__ void load_tile(Staged<D, NW>& st, const ExtendArgs& a,
-                                          const int32_t* bt_row, int npages, int seq_len,
-                                          int kv_head, int tile, int tid) {
-  using S = Shape<D, NW>;
-  int64_t base[S::kPages];  // element offset of (page, kv_head) block, or -1
-#pragma unroll
-  for (int pi = 0; pi < S::kPages; ++pi) {
-    const int lp = tile * S::kPages + pi;
-    int64_t b = -1;
-    if (lp < npages) {
-      const int32_t p = bt_row[lp];
-      if (p >= 0 && p < a.num_pages) {
-        b = ((int64_t)p * a.num_kv_heads + kv_head) * (int64_t)(kPage * D);
-      } else if (tid == 0) {
-        atomicOr(a.error_flags, 1);
-      }
+// Issue this wave's share (page `wave`) of tile `tile` into the given LDS buffers.
+template <int D>
+__device__ __forceinline__ void issue_tile(const Ctx<D>& c, int tile, uint8_t* kb, uint8_t* vb) {
+  using S = ES<D>;
+  const ExtendArgs& a = *c.a;
+  const int lp = tile * 4 + c.wave;
+  int64_t page = 0;
+  if (lp < c.npages) {
+    const int32_t p = c.bt_row[lp];
+    if (p >= 0 && p < a.num_pages) {
+      page = p;
+    } else if (c.lane == 0) {
+      atomicOr(a.error_flags, 1);
     }
-    base[pi] = b;
   }
+  // Pages past the sequence (and invalid ids) are read from page 0, which always
+  // exists; their keys are masked and their V slots zeroed before use.
+  const int64_t blk = (page * a.num_kv_heads + c.kv_head) * (int64_t)S::kPageBytes;
+  const uint8_t* kg = reinterpret_cast<const uint8_t*>(a.k_pool) + blk;
+  const uint8_t* vg = reinterpret_cast<const uint8_t*>(a.v_pool) + blk;
+  uint8_t* kd = kb + c.wave * S::kPageBytes;
+  uint8_t* vd = vb + c.wave * S::kPageBytes;
 #pragma unroll
-  for (int i = 0; i < S::kKPer; ++i) {
-    const int c = tid + i * S::kThreads;
-    const int key = c / (D / 8), part = c % (D / 8);
-    const int64_t b = base[key / kPage];
-    st.k[i] = b >= 0 ? load_u32x4(a.k_pool + b + (key % kPage) * D + part * 8) : zero_u32x4();
-  }
-  const bool tail = (tile + 1) * S::kKeys > seq_len;
-#pragma unroll
-  for (int i = 0; i < S::kVPer; ++i) {
-    const int c = tid + i * S::kThreads;
-    const int pi = c / (D * 2);
-    const int off = (c % (D * 2)) * 8;  // within the page's [D][16] block
-    const int64_t b = base[pi];
-    u32x4 x = b >= 0 ? load_u32x4(a.v_pool + b + off) : zero_u32x4();
-    if (tail) {
-      const int key0 = tile * S::kKeys + pi * kPage + (off & (kPage - 1));
-      x = keep_first(x, seq_len - key0);
-    }
-    st.v[i] = x;
+  for (int i = 0; i < S::kDma; ++i) {
+    __builtin_amdgcn_global_load_lds(kg + c.k_dma_off[i], kd + i * 1024, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(vg + i * 1024 + c.lane * 16, vd + i * 1024, 16, 0, 0);
   }
 }
 
-template <int D, int NW>
-__device__ __forceinline__ void store_tile(const Staged<D, NW>& st, uint16_t* k_lds,
-                                           uint16_t* v_lds, int tid) {
-  using S = Shape<D, NW>;
-#pragma unroll
-  for (int i = 0; i < S::kKPer; ++i) {
-    const int c = tid + i * S::kThreads;
-    const int key = c / (D / 8), part = c % (D / 8);
-    store_u32x4(k_lds + key * S::kKPitch + part * 8, st.k[i]);
-  }
-#pragma unroll
-  for (int i = 0; i < S::kVPer; ++i) {
-    const int c = tid + i * S::kThreads;
-    store_u32x4(v_lds + c * 8, st.v[i]);
+// Zero the V^T slots of keys >= seq_len in a tile (only the last tile of an item).
+template <int D>
+__device__ __forceinline__ void zero_tail(uint8_t* vb, int k0, int seq_len, int tid) {
+  using S = ES<D>;
+  for (int row = tid; row < 4 * D; row += kThreads) {
+    const int pi = row / D, d = row % D;
+    const int nvalid = seq_len - (k0 + pi * kPage);
+    if (nvalid >= kPage) continue;
+    uint16_t* r = reinterpret_cast<uint16_t*>(vb + pi * S::kPageBytes + d * (kPage * 2));
+    for (int s = nvalid < 0 ? 0 : nvalid; s < kPage; ++s) r[s] = 0;
   }
 }
 
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void extend_attn_kernel(ExtendArgs a) {
-  using S = Shape<D, NW>;
-  constexpr int kDC = D / 16;  // 16-wide head-dim chunks of the QK^T contraction
+template <int D>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void extend_attn_kernel(ExtendArgs a) {
+  using S = ES<D>;
+  constexpr int kDC = D / 16;  // 16-wide head-dim chunks of QK^T
   constexpr int kDT = D / 32;  // 32-row head-dim tiles of O^T
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][S::kKTile];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][S::kVTile];
+  __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[S::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t k_lds1[S::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[S::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_lds1[S::kTileBytes];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q = lane & 31, h = lane >> 5;
 
   const ExtendItem it = a.items[blockIdx.x];
   const TaskDesc td = a.tasks[it.task];
   const int P = td.prefix;
   const int seq_len = td.prefix + td.extend;
-  const int npages = (seq_len + kPage - 1) / kPage;
-  const int32_t* bt_row = a.block_table + (int64_t)it.task * a.bt_stride;
   const int G = a.group;
+
+  Ctx<D> c;
+  c.a = &a;
+  c.bt_row = a.block_table + (int64_t)it.task * a.bt_stride;
+  c.npages = (seq_len + kPage - 1) / kPage;
+  c.seq_len = seq_len;
+  c.kv_head = it.kv_head;
+  c.wave = wave;
+  c.lane = lane;
+#pragma unroll
+  for (int i = 0; i < S::kDma; ++i) {
+    const int r = i * S::kRowsPerDma + lane / S::kNG;  // row inside the page (== tile row mod 16)
+    const int g = kswz<D>(r, lane % S::kNG);
+    c.k_dma_off[i] = r * S::kRowBytes + g * 16;
+  }
+
+  // start streaming tile 0 before anything else
+  issue_tile<D>(c, 0, k_lds0, v_lds0);
 
   // this lane's query row: (token tk of the block, head j of the group)
   const int r = wave * 32 + q;
@@ -149,15 +162,22 @@ __global__ __launch_bounds__(NW * 64) void extend_attn_kernel(ExtendArgs a) {
   const int lim = row_valid ? P + it.tok0 + tk : -1;  // last visible key position
   const int64_t qrow = (int64_t)(td.row_start + it.tok0 + tk) * a.num_q_heads +
                        it.kv_head * G + j;
-
   bf16x8 qf[kDC];
 #pragma unroll
-  for (int c = 0; c < kDC; ++c)
-    qf[c] = as_bf16x8(row_valid ? load_u32x4(a.q + qrow * D + 16 * c + 8 * h) : zero_u32x4());
+  for (int cc = 0; cc < kDC; ++cc)
+    qf[cc] = as_bf16x8(row_valid ? load_u32x4(a.q + qrow * D + 16 * cc + 8 * h) : zero_u32x4());
 
-  const int kend = P + it.tok0 + it.ntok;            // keys needed by the last row
-  const int ntiles = (kend + S::kKeys - 1) / S::kKeys;
-  const int n_full = (P + it.tok0 + 1) / S::kKeys;   // tiles every row sees completely
+  // per-lane LDS byte offsets of the MFMA operands
+  const int krow = perm32(q);
+  int k_rd[kDC];
+#pragma unroll
+  for (int cc = 0; cc < kDC; ++cc) k_rd[cc] = krow * S::kRowBytes + kswz<D>(krow, 2 * cc + h) * 16;
+  const int v_rd = krow * (kPage * 2) + h * 16;
+
+  const int kend = P + it.tok0 + it.ntok;           // keys needed by the last row
+  const int ntiles = (kend + 63) / 64;
+  const int n_full = (P + it.tok0 + 1) / 64;        // tiles every row sees completely
+  const float csc = a.scale_log2;
 
   f32x16 o[kDT];
 #pragma unroll
@@ -166,51 +186,32 @@ __global__ __launch_bounds__(NW * 64) void extend_attn_kernel(ExtendArgs a) {
     for (int e = 0; e < 16; ++e) o[t][e] = 0.0f;
   float m_ref = kNoMax, l_part = 0.0f;
 
-  Staged<D, NW> stg;
-  load_tile<D, NW>(stg, a, bt_row, npages, seq_len, it.kv_head, 0, tid);
-  store_tile<D, NW>(stg, k_lds[0], v_lds[0], tid);
-  __syncthreads();
-
-  const int krow = perm32(q);
-  for (int tile = 0; tile < ntiles; ++tile) {
-    const int buf = tile & 1;
-    const bool more = tile + 1 < ntiles;
-    if (more) load_tile<D, NW>(stg, a, bt_row, npages, seq_len, it.kv_head, tile + 1, tid);
-
-    const uint16_t* kl = k_lds[buf];
-    const uint16_t* vl = v_lds[buf];
-
-    // S^T for the two 32-key halves of the tile
+  auto compute = [&](const uint8_t* kb, const uint8_t* vb, int tile) {
     f32x16 s[2];
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[st][e] = 0.0f;
 #pragma unroll
-      for (int c = 0; c < kDC; ++c) {
-        const bf16x8 kf =
-            as_bf16x8(load_u32x4(kl + (st * 32 + krow) * S::kKPitch + 16 * c + 8 * h));
-        s[st] = mfma32(kf, qf[c], s[st]);
+      for (int cc = 0; cc < kDC; ++cc) {
+        const bf16x8 kf = as_bf16x8(load_u32x4(kb + st * 32 * S::kRowBytes + k_rd[cc]));
+        s[st] = mfma32(kf, qf[cc], s[st]);
       }
     }
-
-    // scale, mask, tile max
-    const bool masked = tile >= n_full;
-    const int k0 = tile * S::kKeys;
-    float mt = -INFINITY;
+    if (tile >= n_full) {  // diagonal / tail tile: hide keys past this row's position
+      const int kbase = tile * 64 + 8 * h;
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (kbase + 32 * st + 16 * (e >> 3) + (e & 7) > lim) s[st][e] = -INFINITY;
+    }
+    float mt = s[0][0];
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float x = s[st][e] * a.scale_log2;
-        if (masked) {
-          const int key = k0 + 32 * st + 16 * (e >> 3) + 8 * h + (e & 7);
-          x = key <= lim ? x : -INFINITY;
-        }
-        s[st][e] = x;
-        mt = fmaxf(mt, x);
-      }
-    mt = fmaxf(mt, xor_shfl(mt, 32));
+      for (int e = 0; e < 16; ++e) mt = fmaxf(mt, s[st][e]);
+    mt = fmaxf(mt, xor_shfl(mt, 32)) * csc;
     if (__any(mt > m_ref + kRescaleSlack)) {
       const float m_new = fmaxf(m_ref, mt);
       const float alpha = fast_exp2(m_ref - m_new);
@@ -221,9 +222,7 @@ __global__ __launch_bounds__(NW * 64) void extend_attn_kernel(ExtendArgs a) {
         for (int e = 0; e < 16; ++e) o[t][e] *= alpha;
       m_ref = m_new;
     }
-
-    // probabilities -> bf16 B operands, 8 consecutive keys per lane
-    bf16x8 pb[2][2];
+    const float negm = -m_ref;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
@@ -231,29 +230,33 @@ __global__ __launch_bounds__(NW * 64) void extend_attn_kernel(ExtendArgs a) {
         u32x4 w;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float p0 = fast_exp2(s[st][8 * m + 2 * e] - m_ref);
-          const float p1 = fast_exp2(s[st][8 * m + 2 * e + 1] - m_ref);
+          const float p0 = fast_exp2(fmaf(s[st][8 * m + 2 * e], csc, negm));
+          const float p1 = fast_exp2(fmaf(s[st][8 * m + 2 * e + 1], csc, negm));
           l_part += p0 + p1;
           w[e] = pack_bf16x2(p0, p1);
         }
-        pb[st][m] = as_bf16x8(w);
+        const bf16x8 pb = as_bf16x8(w);
+        const uint8_t* vp = vb + (2 * st + m) * S::kPageBytes + v_rd;
+#pragma unroll
+        for (int t = 0; t < kDT; ++t)
+          o[t] = mfma32(as_bf16x8(load_u32x4(vp + t * 1024)), pb, o[t]);
       }
+  };
 
-    // O^T += V^T . P^T, 16 keys (one page) per MFMA
-#pragma unroll
-    for (int st = 0; st < 2; ++st)
-#pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        const uint16_t* vp = vl + (2 * st + m) * D * kPage + 8 * h;
-#pragma unroll
-        for (int t = 0; t < kDT; ++t) {
-          const bf16x8 vf = as_bf16x8(load_u32x4(vp + (32 * t + krow) * kPage));
-          o[t] = mfma32(vf, pb[st][m], o[t]);
-        }
-      }
+  auto step = [&](int tile, uint8_t* kb, uint8_t* vb, uint8_t* kn, uint8_t* vn) {
+    wait_all_vmem();
+    __syncthreads();  // tile landed for every wave; the other buffer is free again
+    if ((tile + 1) * 64 > seq_len) {
+      zero_tail<D>(vb, tile * 64, seq_len, tid);
+      __syncthreads();
+    }
+    if (tile + 1 < ntiles) issue_tile<D>(c, tile + 1, kn, vn);
+    compute(kb, vb, tile);
+  };
 
-    if (more) store_tile<D, NW>(stg, k_lds[buf ^ 1], v_lds[buf ^ 1], tid);
-    __syncthreads();
+  for (int tile = 0; tile < ntiles; tile += 2) {
+    step(tile, k_lds0, v_lds0, k_lds1, v_lds1);
+    if (tile + 1 < ntiles) step(tile + 1, k_lds1, v_lds1, k_lds0, v_lds0);
   }
 
   const float l_tot = l_part + xor_shfl(l_part, 32);
@@ -274,9 +277,9 @@ __global__ __launch_bounds__(NW * 64) void extend_attn_kernel(ExtendArgs a) {
   }
 }
 
-template <int D, int NW>
+template <int D>
 hipError_t launch(const ExtendArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL((extend_attn_kernel<D, NW>), dim3(a.num_items), dim3(NW * 64), 0, stream, a);
+  hipLaunchKernelGGL((extend_attn_kernel<D>), dim3(a.num_items), dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -284,8 +287,9 @@ hipError_t launch(const ExtendArgs& a, hipStream_t stream) {
 
 hipError_t launch_extend(const ExtendArgs& a, int head_dim, int waves, hipStream_t stream) {
   if (a.num_items == 0) return hipSuccess;
-  if (head_dim == 128 && waves == 4) return launch<128, 4>(a, stream);
-  if (head_dim == 64 && waves == 4) return launch<64, 4>(a, stream);
+  if (waves != kWaves) return hipErrorInvalidValue;
+  if (head_dim == 128) return launch<128>(a, stream);
+  if (head_dim == 64) return launch<64>(a, stream);
   return hipErrorInvalidValue;
 }
 
