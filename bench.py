@@ -47,8 +47,9 @@ def parse_args():
     ap.add_argument("--workload", default="agent_resume_7b")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall-time budget of the oracle CPU baseline sample (0 disables it)")
-    ap.add_argument("--skip-reprefill", action="store_true",
-                    help="leave out stage 4 (for profiling the other kernels only)")
+    ap.add_argument("--reprefill", type=int, default=1,
+                    help="include the recompute comparison (append history + full prefill) "
+                         "for extend workloads (1) or not (0)")
     return ap.parse_args()
 
 
@@ -132,6 +133,67 @@ def cpu_baseline(wl, q_ext_host, budget_s: float):
     return info, outs
 
 
+class Stage:
+    """One timed call of the step: a callable plus its algorithmic work."""
+
+    def __init__(self, name, fn, flops=0.0, bytes_=0.0):
+        self.name, self.fn, self.flops, self.bytes = name, fn, flops, bytes_
+        self.times = []
+
+
+def build_stages(wl, kv, dev, args, torch, np_up):
+    """The step for this workload: the list of stages, in order."""
+    s = wl.spec
+    zeros = np.zeros(wl.num_tasks, np.int32)
+    ones = np.ones(wl.num_tasks, np.int32)
+    stages = []
+    keep = {}
+    if s.kind in ("extend", "long_horizon"):
+        k_ext, v_ext = np_up(wl.packed("k", wl.extend_ranges())), np_up(wl.packed("v", wl.extend_ranges()))
+        q_ext = np_up(wl.packed("q", wl.extend_ranges()))
+        out_ext = torch.empty_like(q_ext)
+        keep.update(q_ext=q_ext, out_ext=out_ext)
+        stages.append(Stage("append_new", lambda: kv.append(k_ext, v_ext, wl.prefix_lens, wl.extend_lens),
+                            bytes_=append_bytes(wl, int(wl.extend_lens.sum()))))
+        stages.append(Stage("extend", lambda: kv.extend(q_ext, wl.prefix_lens, wl.extend_lens, out=out_ext),
+                            flops=extend_flops(wl)))
+    if s.kind == "extend":
+        last = np.cumsum(wl.extend_lens) - 1
+        q_dec = keep["q_ext"][torch.from_numpy(last.astype(np.int64)).to(dev)].contiguous()
+        out_dec = torch.empty_like(q_dec)
+        stages.append(Stage("decode", lambda: kv.decode(q_dec, wl.seq_lens, out=out_dec),
+                            bytes_=decode_bytes(wl, wl.seq_lens)))
+        if args.reprefill:
+            k_full, v_full = np_up(wl.packed("k", wl.full_ranges())), np_up(wl.packed("v", wl.full_ranges()))
+            q_full = np_up(wl.packed("q", wl.full_ranges()))
+            out_full = torch.empty_like(q_full)
+            stages.append(Stage("append_history", lambda: kv.append(k_full, v_full, zeros, wl.seq_lens),
+                                bytes_=append_bytes(wl, int(wl.seq_lens.sum()))))
+            stages.append(Stage("prefill", lambda: kv.prefill(q_full, wl.seq_lens, out=out_full),
+                                flops=prefill_flops(wl)))
+    elif s.kind == "decode":
+        k_new, v_new = np_up(wl.packed("k", wl.extend_ranges())), np_up(wl.packed("v", wl.extend_ranges()))
+        q_dec = np_up(wl.packed("q", wl.extend_ranges()))
+        out_dec = torch.empty_like(q_dec)
+        stages.append(Stage("append_new", lambda: kv.append(k_new, v_new, wl.prefix_lens, wl.extend_lens),
+                            bytes_=append_bytes(wl, wl.num_tasks)))
+        stages.append(Stage("decode", lambda: kv.decode(q_dec, wl.seq_lens, out=out_dec),
+                            bytes_=decode_bytes(wl, wl.seq_lens)))
+    if s.kind == "long_horizon":
+        for step in range(s.decode_steps):
+            rng = wl.decode_ranges(step)
+            pos = (wl.seq_lens + step).astype(np.int32)
+            kn, vn, qn = (np_up(wl.packed(x, rng)) for x in ("k", "v", "q"))
+            on = torch.empty_like(qn)
+            stages.append(Stage("append_decode_%d" % step,
+                                (lambda kn=kn, vn=vn, pos=pos: kv.append(kn, vn, pos, ones)),
+                                bytes_=append_bytes(wl, wl.num_tasks)))
+            stages.append(Stage("decode_%d" % step,
+                                (lambda qn=qn, on=on, pos=pos: kv.decode(qn, pos + 1, out=on)),
+                                bytes_=decode_bytes(wl, pos + 1)))
+    return stages, keep
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -147,118 +209,93 @@ def main():
     dev = torch.device("cuda", 0)
     wl = W.make_workload(args.workload)
     s = wl.spec
-    assert s.kind == "extend", "the benchmark step needs an extend workload"
 
     def up(bits):
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
 
     t_setup = time.time()
-    k_pre = up(wl.packed("k", wl.prefix_ranges()))
-    v_pre = up(wl.packed("v", wl.prefix_ranges()))
-    k_ext = up(wl.packed("k", wl.extend_ranges()))
-    v_ext = up(wl.packed("v", wl.extend_ranges()))
-    q_ext_host = wl.packed("q", wl.extend_ranges())
-    q_ext = up(q_ext_host)
-    k_full = up(wl.packed("k", wl.full_ranges()))
-    v_full = up(wl.packed("v", wl.full_ranges()))
-    q_full = None if args.skip_reprefill else up(wl.packed("q", wl.full_ranges()))
     kv = tide.PagedKV(wl.num_pages, s.num_q_heads, s.num_kv_heads, s.head_dim, wl.block_table,
                       wl.sm_scale, device=dev)
     zeros = np.zeros(wl.num_tasks, np.int32)
-    kv.append(k_pre, v_pre, zeros, wl.prefix_lens)
-    # decode: the last resumed token of each task as the query over its whole context
-    last_rows = np.cumsum(wl.extend_lens) - 1
-    q_dec = q_ext[torch.from_numpy(last_rows.astype(np.int64)).to(dev)].contiguous()
-    out_ext = torch.empty_like(q_ext)
-    out_dec = torch.empty_like(q_dec)
-    out_full = None if q_full is None else torch.empty_like(q_full)
+    if wl.prefix_lens.sum() > 0:
+        kv.append(up(wl.packed("k", wl.prefix_ranges())), up(wl.packed("v", wl.prefix_ranges())),
+                  zeros, wl.prefix_lens)
+    stages, keep = build_stages(wl, kv, dev, args, torch, up)
     torch.cuda.synchronize()
     setup_s = time.time() - t_setup
-
     stream = torch.cuda.current_stream()
-    stages = ["append_new", "extend", "decode"] + ([] if q_full is None else
-                                                   ["append_history", "prefill"])
-    ev = {k: [] for k in stages}
 
     def step(record):
-        marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] if record else None
+        marks = None
         if record:
+            marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
             marks[0].record(stream)
-        kv.append(k_ext, v_ext, wl.prefix_lens, wl.extend_lens)
-        if record:
-            marks[1].record(stream)
-        kv.extend(q_ext, wl.prefix_lens, wl.extend_lens, out=out_ext)
-        if record:
-            marks[2].record(stream)
-        kv.decode(q_dec, wl.seq_lens, out=out_dec)
-        if record:
-            marks[3].record(stream)
-        if q_full is not None:
-            kv.append(k_full, v_full, zeros, wl.seq_lens)
+        for i, st in enumerate(stages):
+            st.fn()
             if record:
-                marks[4].record(stream)
-            kv.prefill(q_full, wl.seq_lens, out=out_full)
-            if record:
-                marks[5].record(stream)
-        if record:
-            for i, k in enumerate(stages):
-                ev[k].append((marks[i], marks[i + 1]))
+                marks[i + 1].record(stream)
+        return marks
 
     for _ in range(args.warmup):
         step(False)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(True)
+    recorded = [step(True) for _ in range(args.steps)]
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms = {k: float(np.mean([a.elapsed_time(b) for a, b in v])) for k, v in ev.items()}
+    for marks in recorded:
+        for i, st in enumerate(stages):
+            st.times.append(marks[i].elapsed_time(marks[i + 1]))
+    ms = {st.name: float(np.mean(st.times)) for st in stages}
 
-    f_ext = extend_flops(wl)
-    ext_tflops = f_ext / (ms["extend"] * 1e-3) / 1e12
-    dec_bytes = decode_bytes(wl, wl.seq_lens)
-    dec_gbs = dec_bytes / (ms["decode"] * 1e-3) / 1e9
-    app_gbs = append_bytes(wl, int(wl.extend_lens.sum())) / (ms["append_new"] * 1e-3) / 1e9
-    extra = {
-        "stage_ms": {k: round(v, 4) for k, v in ms.items()},
-        "extend_tflops": round(ext_tflops, 2),
-        "extend_bf16_peak_frac": round(ext_tflops / PEAK_BF16_TFLOPS, 4),
-        "extend_tokens_per_s": round(float(wl.extend_lens.sum()) / (ms["extend"] * 1e-3), 1),
-        "decode_gbs": round(dec_gbs, 1),
-        "decode_hbm_frac": round(dec_gbs / PEAK_HBM_GBS, 4),
-        "decode_note": "one query per task (its last resumed token) over the whole context",
-        "append_gbs": round(app_gbs, 1),
-        "setup_s": round(setup_s, 1),
-    }
-    rooflines = {
-        "extend": {"bound": "mfma", "achieved": round(ext_tflops, 2), "peak": PEAK_BF16_TFLOPS,
-                   "unit": "TFLOP/s", "frac": round(ext_tflops / PEAK_BF16_TFLOPS, 4)},
-        "decode": {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": PEAK_HBM_GBS,
-                   "unit": "GB/s", "frac": round(dec_gbs / PEAK_HBM_GBS, 4)},
-    }
-    if q_full is not None:
-        f_pre = prefill_flops(wl)
-        pre_tflops = f_pre / (ms["prefill"] * 1e-3) / 1e12
+    def total(prefix):
+        sel = [st for st in stages if st.name.startswith(prefix)]
+        return (sum(np.mean(st.times) for st in sel), sum(st.flops for st in sel),
+                sum(st.bytes for st in sel))
+
+    extra = {"stage_ms": {k: round(v, 4) for k, v in ms.items()}, "setup_s": round(setup_s, 1)}
+    rooflines = {}
+    if "extend" in ms:
+        t, f, _ = total("extend")
+        v = f / (t * 1e-3) / 1e12
+        rooflines["extend"] = {"bound": "mfma", "achieved": round(v, 2), "peak": PEAK_BF16_TFLOPS,
+                               "unit": "TFLOP/s", "frac": round(v / PEAK_BF16_TFLOPS, 4)}
+        extra["extend_tokens_per_s"] = round(float(wl.extend_lens.sum()) / (t * 1e-3), 1)
+    if "prefill" in ms:
+        t, f, _ = total("prefill")
+        v = f / (t * 1e-3) / 1e12
+        rooflines["prefill"] = {"bound": "mfma", "achieved": round(v, 2), "peak": PEAK_BF16_TFLOPS,
+                                "unit": "TFLOP/s", "frac": round(v / PEAK_BF16_TFLOPS, 4)}
         resume = ms["append_new"] + ms["extend"]
         recompute = ms["append_history"] + ms["prefill"]
         extra.update({
-            "prefill_tflops": round(pre_tflops, 2),
-            "prefill_bf16_peak_frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4),
             "speedup_vs_reprefill": round(recompute / resume, 3),
             "speedup_vs_reprefill_attention_only": round(ms["prefill"] / ms["extend"], 3),
-            "flop_ratio_prefill_over_extend": round(f_pre / f_ext, 3),
+            "flop_ratio_prefill_over_extend": round(prefill_flops(wl) / extend_flops(wl), 3),
+            "prefill_tokens_per_s": round(float(wl.seq_lens.sum()) / (ms["prefill"] * 1e-3), 1),
         })
-        rooflines["prefill"] = {"bound": "mfma", "achieved": round(pre_tflops, 2),
-                                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                                "frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4)}
-    roofline = dict(rooflines["extend"])
-    roofline["traffic"] = counter_traffic()
-    roofline["kernel"] = "extend_attn_kernel"
+    if any(k.startswith("decode") for k in ms):
+        t, _, b = total("decode")
+        v = b / (t * 1e-3) / 1e9
+        rooflines["decode"] = {"bound": "hbm", "achieved": round(v, 1), "peak": PEAK_HBM_GBS,
+                               "unit": "GB/s", "frac": round(v / PEAK_HBM_GBS, 4)}
+        n_dec = sum(1 for k in ms if k.startswith("decode"))
+        extra["decode_tokens_per_s"] = round(n_dec * wl.num_tasks / (t * 1e-3), 1)
+    if any(k.startswith("append") for k in ms):
+        t, _, b = total("append")
+        v = b / (t * 1e-3) / 1e9
+        rooflines["append"] = {"bound": "hbm", "achieved": round(v, 1), "peak": PEAK_HBM_GBS,
+                               "unit": "GB/s", "frac": round(v / PEAK_HBM_GBS, 4)}
+
+    primary = "extend" if "extend" in rooflines else "decode"
+    roofline = dict(rooflines[primary])
+    roofline["kernel"] = "extend_attn_kernel" if primary == "extend" else "decode_split_kernel"
+    roofline["traffic"] = counter_traffic() if (primary == "extend" and s.key == "agent_resume_7b") else None
 
     cpu = None
-    if args.cpu_seconds > 0:
-        cpu, outs = cpu_baseline(wl, q_ext_host, args.cpu_seconds)
-        got = out_ext.float().cpu().numpy()
+    if args.cpu_seconds > 0 and "extend" in ms:
+        cpu, outs = cpu_baseline(wl, wl.packed("q", wl.extend_ranges()), args.cpu_seconds)
+        got = keep["out_ext"].float().cpu().numpy()
         errs = [np.abs(got[b] - o) for b, o in outs]
         if errs:
             e = np.concatenate([x.ravel() for x in errs])
@@ -268,8 +305,8 @@ def main():
 
     line = {
         "metric": METRIC,
-        "value": round(ext_tflops, 2),
-        "unit": "TFLOP/s",
+        "value": roofline["achieved"],
+        "unit": roofline["unit"],
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -279,7 +316,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": wl.spec.key, "tasks": wl.num_tasks, "q_heads": s.num_q_heads,
+        "config": {"workload": s.key, "tasks": wl.num_tasks, "q_heads": s.num_q_heads,
                    "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "page_size": s.page_size,
                    "extend_tokens": int(wl.extend_lens.sum()), "context_tokens": int(wl.seq_lens.sum()),
                    "pool_pages": wl.num_pages, "lens_digest": wl.lens_digest()},

@@ -19,7 +19,7 @@
 #include "tide_device.h"
 
 namespace tide {
-namespace {
+namespace kern {
 
 constexpr int kWavesPerBlock = 4;
 
@@ -106,7 +106,7 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_split_kernel(Decod
   f32x4 o[D / 16];
 #pragma unroll
   for (int t = 0; t < D / 16; ++t) o[t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-  float m_ref = kNoMax, l_part = 0.0f;
+  float m_ref = kNoMax, l_part = 0.0f, l_exact = 0.0f;
 
   DecodeRegs<D> cur, nxt;
   load_step<D>(cur, a, bt_row, npages, kv_len, it.kv_head, kbeg, lane);
@@ -138,6 +138,7 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_split_kernel(Decod
       const float m_new = fmaxf(m_ref, mt);
       const float alpha = fast_exp2(m_ref - m_new);
       l_part *= alpha;
+      l_exact *= alpha;
 #pragma unroll
       for (int t = 0; t < D / 16; ++t) o[t] *= alpha;
       m_ref = m_new;
@@ -149,8 +150,9 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_split_kernel(Decod
       for (int e = 0; e < 2; ++e) {
         const float p0 = fast_exp2(s[t][2 * e] - m_ref);
         const float p1 = fast_exp2(s[t][2 * e + 1] - m_ref);
-        l_part += p0 + p1;
         w[2 * t + e] = pack_bf16x2(p0, p1);
+        l_part = add_bf16x2(w[2 * t + e], l_part);
+        l_exact += p0 + p1;
       }
     const bf16x8 pb = as_bf16x8(w);
 #pragma unroll
@@ -160,6 +162,8 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_split_kernel(Decod
 
   float l_tot = l_part + xor_shfl(l_part, 16);
   l_tot += xor_shfl(l_tot, 32);
+  float l_ex = l_exact + xor_shfl(l_exact, 16);
+  l_ex += xor_shfl(l_ex, 32);
   if (col < G) {
     const int64_t slot =
         ((int64_t)it.task * a.num_q_heads + it.kv_head * G + col) * a.max_splits + it.split;
@@ -168,13 +172,27 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_split_kernel(Decod
     for (int t = 0; t < D / 16; ++t)
       *reinterpret_cast<f32x4*>(po + 16 * t + 4 * grp) = o[t];
     if (grp == 0) {
-      f32x2 ml = {m_ref, l_tot};
-      *reinterpret_cast<f32x2*>(a.part_ml + slot * 2) = ml;
+      f32x4 ml = {m_ref, l_tot, l_ex, 0.0f};
+      *reinterpret_cast<f32x4*>(a.part_ml + slot * 4) = ml;
     }
   }
 }
 
-// One wave per (task, query head): combine the task's split partials.
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, xor_shfl(v, m));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += xor_shfl(v, m);
+  return v;
+}
+
+// One wave per (task, query head): combine the task's split partials.  Lane s owns split
+// s for the statistics (max, weights); the partial outputs are then accumulated with
+// every lane covering D/64 head-dim entries and the weights broadcast across the wave.
 template <int D>
 __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_merge_kernel(DecodeArgs a) {
   const int lane = threadIdx.x & 63;
@@ -182,22 +200,38 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_merge_kernel(Decod
   if (row >= (int64_t)a.num_tasks * a.num_q_heads) return;
   const int task = (int)(row / a.num_q_heads);
   const int nsplit = a.tasks[task].aux;
-  const float* ml = a.part_ml + row * a.max_splits * 2;
-  float mx = kNoMax;
-  for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, ml[2 * s]);
+  const float* ml = a.part_ml + row * a.max_splits * 4;
+  const float* po = a.part_o + row * a.max_splits * D;
   constexpr int kPer = D / 64;
+
+  float mx = kNoMax;
+  for (int s = lane; s < nsplit; s += 64) mx = fmaxf(mx, ml[4 * s]);
+  mx = wave_max(mx);
+
   float acc[kPer];
 #pragma unroll
   for (int i = 0; i < kPer; ++i) acc[i] = 0.0f;
-  float lsum = 0.0f;
-  const float* po = a.part_o + row * a.max_splits * D;
-  for (int s = 0; s < nsplit; ++s) {
-    const float wgt = fast_exp2(ml[2 * s] - mx);
-    lsum += wgt * ml[2 * s + 1];
+  float l_round = 0.0f, l_ex = 0.0f;
+  for (int s0 = 0; s0 < nsplit; s0 += 64) {
+    const int s = s0 + lane;
+    float wgt = 0.0f;
+    if (s < nsplit) {
+      const f32x4 st = *reinterpret_cast<const f32x4*>(ml + 4 * s);
+      wgt = fast_exp2(st[0] - mx);
+      l_round += wgt * st[1];
+      l_ex += wgt * st[2];
+    }
+    const int n = min(64, nsplit - s0);
+#pragma unroll 4
+    for (int i = 0; i < n; ++i) {
+      const float wi = __shfl(wgt, i, 64);
+      const float* src = po + (int64_t)(s0 + i) * D + kPer * lane;
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) acc[i] += wgt * po[s * D + kPer * lane + i];
+      for (int k = 0; k < kPer; ++k) acc[k] += wi * src[k];
+    }
   }
-  const float inv = 1.0f / lsum;
+  l_round = wave_sum(l_round);
+  const float inv = 1.0f / l_round;
   uint16_t* orow = a.out + row * D;
   if (kPer == 2) {
     *reinterpret_cast<uint32_t*>(orow + 2 * lane) = pack_bf16x2(acc[0] * inv, acc[kPer - 1] * inv);
@@ -205,7 +239,10 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_merge_kernel(Decod
     const uint32_t w = pack_bf16x2(acc[0] * inv, 0.0f);
     orow[lane] = (uint16_t)(w & 0xFFFFu);
   }
-  if (a.lse && lane == 0) a.lse[row] = (mx + __log2f(lsum)) * kLn2;
+  if (a.lse) {
+    l_ex = wave_sum(l_ex);
+    if (lane == 0) a.lse[row] = (mx + __log2f(l_ex)) * kLn2;
+  }
 }
 
 template <int D>
@@ -226,11 +263,11 @@ hipError_t launch(const DecodeArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-}  // namespace
+}  // namespace kern
 
 hipError_t launch_decode(const DecodeArgs& a, int head_dim, hipStream_t stream) {
-  if (head_dim == 128) return launch<128>(a, stream);
-  if (head_dim == 64) return launch<64>(a, stream);
+  if (head_dim == 128) return kern::launch<128>(a, stream);
+  if (head_dim == 64) return kern::launch<64>(a, stream);
   return hipErrorInvalidValue;
 }
 

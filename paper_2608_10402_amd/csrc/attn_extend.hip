@@ -33,7 +33,7 @@
 #include "tide_device.h"
 
 namespace tide {
-namespace {
+namespace kern {
 
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
@@ -71,36 +71,34 @@ struct Ctx {
   int wave;
   int lane;
   int k_dma_off[ES<D>::kDma];  // this lane's source offset inside a K page, per transfer
-};
 
-// Issue this wave's share (page `wave`) of tile `tile` into the given LDS buffers.
-template <int D>
-__device__ __forceinline__ void issue_tile(const Ctx<D>& c, int tile, uint8_t* kb, uint8_t* vb) {
-  using S = ES<D>;
-  const ExtendArgs& a = *c.a;
-  const int lp = tile * 4 + c.wave;
-  int64_t page = 0;
-  if (lp < c.npages) {
-    const int32_t p = c.bt_row[lp];
-    if (p >= 0 && p < a.num_pages) {
-      page = p;
-    } else if (c.lane == 0) {
-      atomicOr(a.error_flags, 1);
+  // Issue this wave's share (page `wave`) of tile `tile` into the given LDS buffers.
+  __device__ __forceinline__ void issue_tile(int tile, uint8_t* kb, uint8_t* vb) const {
+    using S = ES<D>;
+    const int lp = tile * 4 + wave;
+    int64_t page = 0;
+    if (lp < npages) {
+      const int32_t p = bt_row[lp];
+      if (p >= 0 && p < a->num_pages) {
+        page = p;
+      } else if (lane == 0) {
+        atomicOr(a->error_flags, 1);
+      }
+    }
+    // Pages past the sequence (and invalid ids) are read from page 0, which always
+    // exists; their keys are masked and their V slots zeroed before use.
+    const int64_t blk = (page * a->num_kv_heads + kv_head) * (int64_t)S::kPageBytes;
+    const uint8_t* kg = reinterpret_cast<const uint8_t*>(a->k_pool) + blk;
+    const uint8_t* vg = reinterpret_cast<const uint8_t*>(a->v_pool) + blk;
+    uint8_t* kd = kb + wave * S::kPageBytes;
+    uint8_t* vd = vb + wave * S::kPageBytes;
+#pragma unroll
+    for (int i = 0; i < S::kDma; ++i) {
+      __builtin_amdgcn_global_load_lds(kg + k_dma_off[i], kd + i * 1024, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vg + i * 1024 + lane * 16, vd + i * 1024, 16, 0, 0);
     }
   }
-  // Pages past the sequence (and invalid ids) are read from page 0, which always
-  // exists; their keys are masked and their V slots zeroed before use.
-  const int64_t blk = (page * a.num_kv_heads + c.kv_head) * (int64_t)S::kPageBytes;
-  const uint8_t* kg = reinterpret_cast<const uint8_t*>(a.k_pool) + blk;
-  const uint8_t* vg = reinterpret_cast<const uint8_t*>(a.v_pool) + blk;
-  uint8_t* kd = kb + c.wave * S::kPageBytes;
-  uint8_t* vd = vb + c.wave * S::kPageBytes;
-#pragma unroll
-  for (int i = 0; i < S::kDma; ++i) {
-    __builtin_amdgcn_global_load_lds(kg + c.k_dma_off[i], kd + i * 1024, 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(vg + i * 1024 + c.lane * 16, vd + i * 1024, 16, 0, 0);
-  }
-}
+};
 
 // Zero the V^T slots of keys >= seq_len in a tile (only the last tile of an item).
 template <int D>
@@ -115,7 +113,10 @@ __device__ __forceinline__ void zero_tail(uint8_t* vb, int k0, int seq_len, int 
   }
 }
 
-template <int D>
+// kLse: also keep the exact fp32 sum of the probabilities, so the returned log-sum-exp is
+// the true one; the output itself is normalised by the sum of the bf16-rounded weights
+// that the P.V product used.
+template <int D, bool kLse>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void extend_attn_kernel(ExtendArgs a) {
   using S = ES<D>;
@@ -153,7 +154,7 @@ void extend_attn_kernel(ExtendArgs a) {
   }
 
   // start streaming tile 0 before anything else
-  issue_tile<D>(c, 0, k_lds0, v_lds0);
+  c.issue_tile(0, k_lds0, v_lds0);
 
   // this lane's query row: (token tk of the block, head j of the group)
   const int r = wave * 32 + q;
@@ -184,7 +185,7 @@ void extend_attn_kernel(ExtendArgs a) {
   for (int t = 0; t < kDT; ++t)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[t][e] = 0.0f;
-  float m_ref = kNoMax, l_part = 0.0f;
+  float m_ref = kNoMax, l_part = 0.0f, l_exact = 0.0f;
 
   auto compute = [&](const uint8_t* kb, const uint8_t* vb, int tile) {
     f32x16 s[2];
@@ -216,6 +217,7 @@ void extend_attn_kernel(ExtendArgs a) {
       const float m_new = fmaxf(m_ref, mt);
       const float alpha = fast_exp2(m_ref - m_new);
       l_part *= alpha;
+      if (kLse) l_exact *= alpha;
 #pragma unroll
       for (int t = 0; t < kDT; ++t)
 #pragma unroll
@@ -223,6 +225,7 @@ void extend_attn_kernel(ExtendArgs a) {
       m_ref = m_new;
     }
     const float negm = -m_ref;
+    float lt = 0.0f, le = 0.0f;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
@@ -232,8 +235,9 @@ void extend_attn_kernel(ExtendArgs a) {
         for (int e = 0; e < 4; ++e) {
           const float p0 = fast_exp2(fmaf(s[st][8 * m + 2 * e], csc, negm));
           const float p1 = fast_exp2(fmaf(s[st][8 * m + 2 * e + 1], csc, negm));
-          l_part += p0 + p1;
           w[e] = pack_bf16x2(p0, p1);
+          lt = add_bf16x2(w[e], lt);
+          if (kLse) le += p0 + p1;
         }
         const bf16x8 pb = as_bf16x8(w);
         const uint8_t* vp = vb + (2 * st + m) * S::kPageBytes + v_rd;
@@ -241,6 +245,8 @@ void extend_attn_kernel(ExtendArgs a) {
         for (int t = 0; t < kDT; ++t)
           o[t] = mfma32(as_bf16x8(load_u32x4(vp + t * 1024)), pb, o[t]);
       }
+    l_part += lt;  // short dot2 chains per tile, IEEE adds across tiles
+    if (kLse) l_exact += le;
   };
 
   auto step = [&](int tile, uint8_t* kb, uint8_t* vb, uint8_t* kn, uint8_t* vn) {
@@ -250,7 +256,7 @@ void extend_attn_kernel(ExtendArgs a) {
       zero_tail<D>(vb, tile * 64, seq_len, tid);
       __syncthreads();
     }
-    if (tile + 1 < ntiles) issue_tile<D>(c, tile + 1, kn, vn);
+    if (tile + 1 < ntiles) c.issue_tile(tile + 1, kn, vn);
     compute(kb, vb, tile);
   };
 
@@ -273,23 +279,36 @@ void extend_attn_kernel(ExtendArgs a) {
           w[e] = pack_bf16x2(o[t][8 * half + 2 * e] * inv, o[t][8 * half + 2 * e + 1] * inv);
         store_u32x4(orow + 32 * t + 16 * half + 8 * h, w);
       }
-    if (a.lse && h == 0) a.lse[qrow] = (m_ref + __log2f(l_tot)) * kLn2;
+    if (kLse) {
+      const float l_ex = l_exact + xor_shfl(l_exact, 32);
+      if (h == 0) a.lse[qrow] = (m_ref + __log2f(l_ex)) * kLn2;
+    }
   }
 }
 
 template <int D>
 hipError_t launch(const ExtendArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL((extend_attn_kernel<D>), dim3(a.num_items), dim3(kThreads), 0, stream, a);
+  if (a.lse)
+    hipLaunchKernelGGL((extend_attn_kernel<D, true>), dim3(a.num_items), dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((extend_attn_kernel<D, false>), dim3(a.num_items), dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
-}  // namespace
+// Both variants of each head size are instantiated explicitly: the host pass otherwise
+// emits the launch stub of only one of two specialisations that differ in the bool.
+template __global__ void extend_attn_kernel<128, false>(ExtendArgs);
+template __global__ void extend_attn_kernel<128, true>(ExtendArgs);
+template __global__ void extend_attn_kernel<64, false>(ExtendArgs);
+template __global__ void extend_attn_kernel<64, true>(ExtendArgs);
+
+}  // namespace kern
 
 hipError_t launch_extend(const ExtendArgs& a, int head_dim, int waves, hipStream_t stream) {
   if (a.num_items == 0) return hipSuccess;
-  if (waves != kWaves) return hipErrorInvalidValue;
-  if (head_dim == 128) return launch<128>(a, stream);
-  if (head_dim == 64) return launch<64>(a, stream);
+  if (waves != kern::kWaves) return hipErrorInvalidValue;
+  if (head_dim == 128) return kern::launch<128>(a, stream);
+  if (head_dim == 64) return kern::launch<64>(a, stream);
   return hipErrorInvalidValue;
 }
 

@@ -13,7 +13,7 @@
 #include "tide_device.h"
 
 namespace tide {
-namespace {
+namespace kern {
 
 constexpr int kWaves = 4;
 
@@ -63,12 +63,12 @@ hipError_t launch(const AppendArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-}  // namespace
+}  // namespace kern
 
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
   if (a.num_items == 0) return hipSuccess;
-  if (a.head_dim == 128) return launch<128>(a, stream);
-  if (a.head_dim == 64) return launch<64>(a, stream);
+  if (a.head_dim == 128) return kern::launch<128>(a, stream);
+  if (a.head_dim == 64) return kern::launch<64>(a, stream);
   return hipErrorInvalidValue;
 }
 

@@ -210,7 +210,7 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
     plan->part_o_off = off;
     off = align_up(off + slots * dims.head_dim * sizeof(float), kWsAlign);
     plan->part_ml_off = off;
-    off = align_up(off + slots * 2 * sizeof(float), kWsAlign);
+    off = align_up(off + slots * 4 * sizeof(float), kWsAlign);
   }
   plan->total_bytes = off;
 

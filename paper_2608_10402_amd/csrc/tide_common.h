@@ -106,7 +106,8 @@ struct DecodeArgs {
   const TaskDesc* tasks;  // prefix + extend == kv_len, aux == number of splits
   const DecodeItem* items;
   float* part_o;   // [num_tasks][Hq][max_splits][d] unnormalised partial outputs
-  float* part_ml;  // [num_tasks][Hq][max_splits][2] (running max in base-2 units, sum)
+  float* part_ml;  // [num_tasks][Hq][max_splits][4]: max (base-2 units), sum of the
+                   // bf16-rounded weights, exact fp32 sum, unused
   uint16_t* out;
   float* lse;
   int32_t* error_flags;

@@ -48,6 +48,14 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// acc + lo + hi of a packed bf16 pair (v_dot2c_f32_bf16 against (1, 1)).  Summing the
+// rounded probabilities keeps the softmax denominator consistent with the bf16 weights
+// the P.V product actually uses, at half a VALU instruction per probability.
+__device__ __forceinline__ float add_bf16x2(uint32_t packed, float acc) {
+  const bf16x2 one = __builtin_bit_cast(bf16x2, 0x3F803F80u);  // (1.0, 1.0)
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, packed), one, acc, false);
+}
+
 __device__ __forceinline__ float xor_shfl(float v, int mask) {
   return __shfl_xor(v, mask, 64);
 }

@@ -1,0 +1,163 @@
+"""The C ABI on the CPU: libtide.so loads, exports exactly what include/tide.h declares,
+and rejects bad arguments with the documented status codes before touching a GPU.
+
+No call here launches work: every call fails validation (or is a no-op) on the host.
+"""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import paper_2608_10402_amd as tide
+from paper_2608_10402_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tide.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"TIDE_API\s+[\w\s\*]+?\b(tide_\w+)\s*\(", text)))
+
+
+def exported_functions():
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], check=True,
+                         capture_output=True, text=True).stdout
+    return sorted(l.split()[-1] for l in out.splitlines() if " T " in l)
+
+
+def test_library_exports_exactly_the_header():
+    lib = tide.load()
+    decl = declared_functions()
+    assert decl == sorted(_lib.EXPORTED)
+    assert exported_functions() == decl
+    for name in decl:
+        assert hasattr(lib, name)
+
+
+def test_header_compiles_as_c():
+    src = '#include "tide.h"\nint main(void) { tide_dims d = {8, 2, 64, 16, 0.125f}; (void)d; return 0; }\n'
+    r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"),
+                        "-x", "c", "-", "-fsyntax-only"], input=src, text=True, capture_output=True)
+    assert r.returncode == 0, r.stderr
+
+
+def test_status_strings():
+    for code in (0, -1, -2, -3, -4, -5):
+        assert tide.status_string(code) and tide.status_string(code) != "unknown status"
+    assert tide.status_string(42) == "unknown status"
+
+
+def _ws(op, a, b, dims, splits=0):
+    lib = tide.load()
+    arr_a = None if a is None else np.ascontiguousarray(a, np.int32)
+    arr_b = None if b is None else np.ascontiguousarray(b, np.int32)
+    n = 0 if arr_a is None else arr_a.size
+    out = ctypes.c_size_t(0)
+    rc = lib.tide_workspace_size(op, n, None if arr_a is None else arr_a.ctypes.data,
+                                 None if arr_b is None else arr_b.ctypes.data,
+                                 ctypes.byref(dims) if dims is not None else None, splits,
+                                 ctypes.byref(out))
+    return rc, out.value
+
+
+GOOD = _lib.make_dims(28, 4, 128, 1 / math.sqrt(128))
+
+
+@pytest.mark.parametrize("dims,code", [
+    (_lib.make_dims(8, 2, 96, 0.1), tide.TIDE_ERR_UNSUPPORTED),      # head_dim 96
+    (_lib.make_dims(8, 3, 64, 0.1), tide.TIDE_ERR_UNSUPPORTED),      # 8 % 3 != 0
+    (_lib.make_dims(34, 2, 64, 0.1), tide.TIDE_ERR_UNSUPPORTED),     # group 17 > 16
+    (_lib.make_dims(8, 2, 64, 0.1, page_size=32), tide.TIDE_ERR_UNSUPPORTED),
+    (_lib.make_dims(0, 2, 64, 0.1), tide.TIDE_ERR_INVALID_ARG),
+    (_lib.make_dims(8, 2, 64, 0.0), tide.TIDE_ERR_INVALID_ARG),
+    (_lib.make_dims(8, 2, 64, float("nan")), tide.TIDE_ERR_INVALID_ARG),
+    (_lib.make_dims(8, 2, 64, float("inf")), tide.TIDE_ERR_INVALID_ARG),
+    (None, tide.TIDE_ERR_INVALID_ARG),
+])
+def test_dims_validation(dims, code):
+    rc, _ = _ws(tide.TIDE_OP_EXTEND, [10], [5], dims)
+    assert rc == code
+
+
+def test_length_validation():
+    assert _ws(tide.TIDE_OP_EXTEND, [10, -1], [5, 5], GOOD)[0] == tide.TIDE_ERR_INVALID_ARG
+    assert _ws(tide.TIDE_OP_EXTEND, [10], [-5], GOOD)[0] == tide.TIDE_ERR_INVALID_ARG
+    assert _ws(tide.TIDE_OP_EXTEND, [10], None, GOOD)[0] == tide.TIDE_ERR_INVALID_ARG
+    assert _ws(tide.TIDE_OP_DECODE, [10, 0], None, GOOD)[0] == tide.TIDE_ERR_INVALID_ARG
+    assert _ws(tide.TIDE_OP_DECODE, [10], None, GOOD, splits=-1)[0] == tide.TIDE_ERR_INVALID_ARG
+    assert _ws(tide.TIDE_OP_EXTEND, [2**31 - 10], [100], GOOD)[0] == tide.TIDE_ERR_INVALID_ARG
+    assert _ws(99, [1], [1], GOOD)[0] == tide.TIDE_ERR_INVALID_ARG
+
+
+def test_workspace_sizes_are_consistent():
+    rc, a = _ws(tide.TIDE_OP_EXTEND, [100, 2000], [10, 300], GOOD)
+    assert rc == 0 and a > 0
+    rc, b = _ws(tide.TIDE_OP_EXTEND, [100, 2000], [10, 3000], GOOD)
+    assert rc == 0 and b >= a  # more rows, more work items
+    rc, p = _ws(tide.TIDE_OP_FULL_PREFILL, [110, 2300], None, GOOD)
+    assert rc == 0 and p > 0
+    rc, d1 = _ws(tide.TIDE_OP_DECODE, [5000, 9000], None, GOOD, splits=1)
+    rc2, d8 = _ws(tide.TIDE_OP_DECODE, [5000, 9000], None, GOOD, splits=8)
+    assert rc == 0 and rc2 == 0 and d8 > d1  # partials grow with the split count
+    rc, z = _ws(tide.TIDE_OP_EXTEND, [], [], GOOD)
+    assert rc == 0 and z > 0  # header only
+
+
+def _call_extend(**over):
+    lib = tide.load()
+    args = dict(q=1, k=1, v=1, pages=10, bt=1, stride=4, n=1, p=[3], e=[2], dims=GOOD, out=1,
+                lse=None, ws=1, ws_bytes=1 << 20)
+    args.update(over)
+    p = np.ascontiguousarray(args["p"], np.int32)
+    e = np.ascontiguousarray(args["e"], np.int32)
+    return lib.tide_extend_attn(args["q"], args["k"], args["v"], args["pages"], args["bt"],
+                                args["stride"], args["n"], p.ctypes.data, e.ctypes.data,
+                                ctypes.byref(args["dims"]) if args["dims"] else None, args["out"],
+                                args["lse"], args["ws"], args["ws_bytes"], None)
+
+
+def test_entry_point_validation_without_gpu():
+    # each of these fails (or is a no-op) before any HIP call
+    assert _call_extend(n=0) == tide.TIDE_OK                              # no tasks: no-op
+    assert _call_extend(e=[0]) == tide.TIDE_OK                            # no rows: no-op
+    assert _call_extend(n=-1) == tide.TIDE_ERR_INVALID_ARG
+    assert _call_extend(q=None) == tide.TIDE_ERR_INVALID_ARG
+    assert _call_extend(out=None) == tide.TIDE_ERR_INVALID_ARG
+    assert _call_extend(ws=None) == tide.TIDE_ERR_INVALID_ARG
+    assert _call_extend(pages=0) == tide.TIDE_ERR_INVALID_ARG
+    assert _call_extend(stride=0) == tide.TIDE_ERR_INVALID_ARG
+    assert _call_extend(p=[60], e=[10]) == tide.TIDE_ERR_CAPACITY          # 70 tokens > 4 pages
+    assert _call_extend(ws_bytes=16) == tide.TIDE_ERR_CAPACITY
+    assert _call_extend(dims=_lib.make_dims(8, 2, 80, 0.1)) == tide.TIDE_ERR_UNSUPPORTED
+    assert _call_extend(p=[-1]) == tide.TIDE_ERR_INVALID_ARG
+
+
+def test_other_entry_points_validation_without_gpu():
+    lib = tide.load()
+    one = np.array([1], np.int32)
+    bad = np.array([0], np.int32)
+    d = ctypes.byref(GOOD)
+    assert lib.tide_decode_attn(1, 1, 1, 10, 1, 4, 1, bad.ctypes.data, d, 0, 1, None, 1, 1 << 20,
+                                None) == tide.TIDE_ERR_INVALID_ARG       # kv_len 0
+    assert lib.tide_decode_attn(1, 1, 1, 10, 1, 4, 0, None, d, 0, 1, None, 1, 0,
+                                None) == tide.TIDE_OK                     # no tasks
+    assert lib.tide_decode_attn(1, 1, 1, 10, 1, 4, 1, one.ctypes.data, d, -2, 1, None, 1, 1 << 20,
+                                None) == tide.TIDE_ERR_INVALID_ARG       # negative splits
+    assert lib.tide_full_prefill_attn(1, 1, 1, 10, 1, 4, 1, np.array([65], np.int32).ctypes.data,
+                                      d, 1, None, 1, 1 << 20, None) == tide.TIDE_ERR_CAPACITY
+    assert lib.tide_kv_append(None, 1, 1, 1, 10, 1, 4, 1, one.ctypes.data, one.ctypes.data, d, 1,
+                              1 << 20, None) == tide.TIDE_ERR_INVALID_ARG
+    assert lib.tide_kv_append(1, 1, 1, 1, 10, 1, 4, 1, one.ctypes.data, bad.ctypes.data, d, 1,
+                              1 << 20, None) == tide.TIDE_OK              # nothing to append
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    q = torch.zeros(4, 8, 64, dtype=torch.bfloat16)
+    with pytest.raises((ValueError, TypeError)):
+        tide.tide_extend_attn(q, q, q, q, [1], [1], _lib.make_dims(8, 2, 64, 0.1), q)
