@@ -20,7 +20,7 @@
 //     O^T += V^T.P^T MFMA with no shuffle.  V pages are stored transposed in the pool
 //     (head-dim major, 16 token slots contiguous), so V^T operands are plain 16-byte LDS
 //     reads.  K rows are XOR-swizzled by 16-byte granule in LDS so that the 64 lanes of an
-//     operand read hit distinct banks.
+//     operand read hit distinct banks; V^T rows swap their 16-byte halves every 8 rows.
 //   * Scores stay raw until one FMA applies sm_scale*log2(e) and subtracts the running
 //     max before v_exp_f32.  The running max is only raised when a tile exceeds it by
 //     more than kRescaleSlack, so the O rescale is skipped on almost every tile.
@@ -56,6 +56,10 @@ __device__ __forceinline__ int kswz(int r, int g) {
   return g ^ ((r / ES<D>::kRB) % ES<D>::kNG);
 }
 
+// Position (0/1) of 16-byte half `hh` of V^T row d in LDS: rows d and d+8 share banks,
+// so the halves of rows with bit 3 set are swapped.
+__device__ __forceinline__ int vswz(int d, int hh) { return hh ^ ((d >> 3) & 1); }
+
 __device__ __forceinline__ void wait_all_vmem() {
   // s_waitcnt vmcnt(0) (gfx9 encoding: expcnt and lgkmcnt left at their maxima)
   __builtin_amdgcn_s_waitcnt(0x0F70);
@@ -63,39 +67,47 @@ __device__ __forceinline__ void wait_all_vmem() {
 
 template <int D>
 struct Ctx {
-  const ExtendArgs* a;
+  const uint8_t* k_pool;
+  const uint8_t* v_pool;
+  int32_t* error_flags;
+  int64_t num_pages;
+  int num_kv_heads;
   const int32_t* bt_row;
   int npages;
   int seq_len;
   int kv_head;
   int wave;
   int lane;
-  int k_dma_off[ES<D>::kDma];  // this lane's source offset inside a K page, per transfer
+  uint32_t k_dma_off[ES<D>::kDma];  // this lane's source offset inside a K page, per transfer
+  uint32_t v_dma_off[ES<D>::kDma];  // same for the V^T page
 
-  // Issue this wave's share (page `wave`) of tile `tile` into the given LDS buffers.
-  __device__ __forceinline__ void issue_tile(int tile, uint8_t* kb, uint8_t* vb) const {
-    using S = ES<D>;
+  // Block-table word of this wave's page (page `wave`) of tile `tile`, loaded as a vector
+  // value: it is issued one tile ahead and only read after the next vmcnt(0), so the
+  // memory round trip overlaps a whole tile of compute instead of stalling the issue.
+  __device__ __forceinline__ int32_t fetch_page(int tile) const {
     const int lp = tile * 4 + wave;
-    int64_t page = 0;
-    if (lp < npages) {
-      const int32_t p = bt_row[lp];
-      if (p >= 0 && p < a->num_pages) {
-        page = p;
-      } else if (lane == 0) {
-        atomicOr(a->error_flags, 1);
-      }
-    }
+    return lp < npages ? bt_row[lp] : 0;
+  }
+
+  // Issue this wave's share of a tile, whose page id `word` came from fetch_page().
+  __device__ __forceinline__ void issue_tile(int32_t word, uint8_t* kb, uint8_t* vb) const {
+    using S = ES<D>;
+    // One word for the whole wave: kept scalar, as is all the address math below.
+    const int32_t p = __builtin_amdgcn_readfirstlane(word);
+    const bool bad = p < 0 || p >= num_pages;
+    const int64_t page = bad ? 0 : p;
+    if (bad && lane == 0) atomicOr(error_flags, 1);
     // Pages past the sequence (and invalid ids) are read from page 0, which always
     // exists; their keys are masked and their V slots zeroed before use.
-    const int64_t blk = (page * a->num_kv_heads + kv_head) * (int64_t)S::kPageBytes;
-    const uint8_t* kg = reinterpret_cast<const uint8_t*>(a->k_pool) + blk;
-    const uint8_t* vg = reinterpret_cast<const uint8_t*>(a->v_pool) + blk;
+    const int64_t blk = (page * num_kv_heads + kv_head) * (int64_t)S::kPageBytes;
+    const uint8_t* kg = k_pool + blk;
+    const uint8_t* vg = v_pool + blk;
     uint8_t* kd = kb + wave * S::kPageBytes;
     uint8_t* vd = vb + wave * S::kPageBytes;
 #pragma unroll
     for (int i = 0; i < S::kDma; ++i) {
       __builtin_amdgcn_global_load_lds(kg + k_dma_off[i], kd + i * 1024, 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vg + i * 1024 + lane * 16, vd + i * 1024, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vg + v_dma_off[i], vd + i * 1024, 16, 0, 0);
     }
   }
 };
@@ -108,8 +120,9 @@ __device__ __forceinline__ void zero_tail(uint8_t* vb, int k0, int seq_len, int 
     const int pi = row / D, d = row % D;
     const int nvalid = seq_len - (k0 + pi * kPage);
     if (nvalid >= kPage) continue;
-    uint16_t* r = reinterpret_cast<uint16_t*>(vb + pi * S::kPageBytes + d * (kPage * 2));
-    for (int s = nvalid < 0 ? 0 : nvalid; s < kPage; ++s) r[s] = 0;
+    uint8_t* r = vb + pi * S::kPageBytes + d * (kPage * 2);
+    for (int s = nvalid < 0 ? 0 : nvalid; s < kPage; ++s)
+      *reinterpret_cast<uint16_t*>(r + vswz(d, s >> 3) * 16 + (s & 7) * 2) = 0;
   }
 }
 
@@ -133,13 +146,18 @@ void extend_attn_kernel(ExtendArgs a) {
   const int q = lane & 31, h = lane >> 5;
 
   const ExtendItem it = a.items[blockIdx.x];
+  if (it.ntok == 0) return;  // padding slot of the XCD-interleaved work list
   const TaskDesc td = a.tasks[it.task];
   const int P = td.prefix;
   const int seq_len = td.prefix + td.extend;
   const int G = a.group;
 
   Ctx<D> c;
-  c.a = &a;
+  c.k_pool = reinterpret_cast<const uint8_t*>(a.k_pool);
+  c.v_pool = reinterpret_cast<const uint8_t*>(a.v_pool);
+  c.error_flags = a.error_flags;
+  c.num_pages = a.num_pages;
+  c.num_kv_heads = a.num_kv_heads;
   c.bt_row = a.block_table + (int64_t)it.task * a.bt_stride;
   c.npages = (seq_len + kPage - 1) / kPage;
   c.seq_len = seq_len;
@@ -150,11 +168,14 @@ void extend_attn_kernel(ExtendArgs a) {
   for (int i = 0; i < S::kDma; ++i) {
     const int r = i * S::kRowsPerDma + lane / S::kNG;  // row inside the page (== tile row mod 16)
     const int g = kswz<D>(r, lane % S::kNG);
-    c.k_dma_off[i] = r * S::kRowBytes + g * 16;
+    c.k_dma_off[i] = (uint32_t)(r * S::kRowBytes + g * 16);
+    const int d = i * 32 + lane / 2;  // V^T row (head-dim entry) this lane's granule lands in
+    c.v_dma_off[i] = (uint32_t)(d * (kPage * 2) + vswz(d, lane & 1) * 16);
   }
 
   // start streaming tile 0 before anything else
-  c.issue_tile(0, k_lds0, v_lds0);
+  c.issue_tile(c.fetch_page(0), k_lds0, v_lds0);
+  int32_t next_page = c.fetch_page(1);  // page id of the tile the next step streams in
 
   // this lane's query row: (token tk of the block, head j of the group)
   const int r = wave * 32 + q;
@@ -173,7 +194,7 @@ void extend_attn_kernel(ExtendArgs a) {
   int k_rd[kDC];
 #pragma unroll
   for (int cc = 0; cc < kDC; ++cc) k_rd[cc] = krow * S::kRowBytes + kswz<D>(krow, 2 * cc + h) * 16;
-  const int v_rd = krow * (kPage * 2) + h * 16;
+  const int v_rd = krow * (kPage * 2) + vswz(krow, h) * 16;
 
   const int kend = P + it.tok0 + it.ntok;           // keys needed by the last row
   const int ntiles = (kend + 63) / 64;
@@ -189,15 +210,29 @@ void extend_attn_kernel(ExtendArgs a) {
 
   auto compute = [&](const uint8_t* kb, const uint8_t* vb, int tile) {
     f32x16 s[2];
+    {
+      u32x4 kf[2][kDC];
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
+      for (int st = 0; st < 2; ++st)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) s[st][e] = 0.0f;
+        for (int cc = 0; cc < kDC; ++cc)
+          kf[st][cc] = load_u32x4(kb + st * 32 * S::kRowBytes + k_rd[cc]);
 #pragma unroll
-      for (int cc = 0; cc < kDC; ++cc) {
-        const bf16x8 kf = as_bf16x8(load_u32x4(kb + st * 32 * S::kRowBytes + k_rd[cc]));
-        s[st] = mfma32(kf, qf[cc], s[st]);
+      for (int st = 0; st < 2; ++st) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s[st][e] = 0.0f;
+#pragma unroll
+        for (int cc = 0; cc < kDC; ++cc) s[st] = mfma32(as_bf16x8(kf[st][cc]), qf[cc], s[st]);
       }
+      // Keep kDC operand reads in flight ahead of the MFMAs: all reads of the first
+      // half, then MFMA/read pairs, then the last MFMAs.
+      __builtin_amdgcn_sched_group_barrier(0x100, kDC, 0);
+#pragma unroll
+      for (int i = 0; i < kDC; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, kDC, 0);
     }
     if (tile >= n_full) {  // diagonal / tail tile: hide keys past this row's position
       const int kbase = tile * 64 + 8 * h;
@@ -256,7 +291,10 @@ void extend_attn_kernel(ExtendArgs a) {
       zero_tail<D>(vb, tile * 64, seq_len, tid);
       __syncthreads();
     }
-    if (tile + 1 < ntiles) c.issue_tile(tile + 1, kn, vn);
+    if (tile + 1 < ntiles) {
+      c.issue_tile(next_page, kn, vn);
+      next_page = c.fetch_page(tile + 2);
+    }
     compute(kb, vb, tile);
   };
 

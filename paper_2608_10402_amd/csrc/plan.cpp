@@ -126,35 +126,60 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
     const int32_t tb = waves * 32 / group;  // tokens per item: waves*32 rows of (token, head)
     plan->waves = waves;
     plan->tokens_per_item = tb;
-    struct Costed {
+    // Work units are (task, kv head): all query blocks of a unit read the same K/V.
+    // Workgroups are dispatched round-robin over the XCDs (item i runs on XCD i % 8),
+    // each with its own L2.  Every unit is placed on one XCD, its blocks consecutive in
+    // that XCD's order, so the blocks that walk the same K/V run side by side and share
+    // it through L2 instead of re-reading HBM.  Units go longest first to the least
+    // loaded XCD; inside a unit the longest blocks go first.
+    struct Unit {
       int64_t cost;
-      ExtendItem it;
+      int32_t task, kv_head;
     };
-    std::vector<Costed> items;
+    std::vector<Unit> units;
     for (int32_t b = 0; b < num_tasks; ++b) {
       const int32_t p = tasks[b].prefix, e = tasks[b].extend;
+      if (e == 0) continue;
+      int64_t cost = 0;
       for (int32_t t0 = 0; t0 < e; t0 += tb) {
         const int32_t n = std::min(tb, e - t0);
-        const int64_t keys = (int64_t)p + t0 + n;
-        for (int32_t g = 0; g < dims.num_kv_heads; ++g) {
-          Costed c;
-          c.cost = keys;
-          c.it.task = b;
-          c.it.kv_head = g;
-          c.it.tok0 = t0;
-          c.it.ntok = n;
-          items.push_back(c);
-        }
+        cost += (int64_t)n * ((int64_t)p + t0 + n);
       }
+      for (int32_t g = 0; g < dims.num_kv_heads; ++g) units.push_back({cost, b, g});
     }
-    // Longest first, so the short items fill in behind the long ones at the end.
-    std::stable_sort(items.begin(), items.end(),
-                     [](const Costed& x, const Costed& y) { return x.cost > y.cost; });
+    std::stable_sort(units.begin(), units.end(),
+                     [](const Unit& x, const Unit& y) { return x.cost > y.cost; });
+    std::vector<std::vector<ExtendItem>> queues(kXcds);
+    std::vector<int64_t> load(kXcds, 0);
+    for (const Unit& u : units) {
+      const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+      load[x] += u.cost;
+      const int32_t p = tasks[u.task].prefix, e = tasks[u.task].extend;
+      const int32_t nblk = (e + tb - 1) / tb;
+      for (int32_t k = nblk - 1; k >= 0; --k) {  // later blocks see more keys
+        ExtendItem it;
+        it.task = u.task;
+        it.kv_head = u.kv_head;
+        it.tok0 = k * tb;
+        it.ntok = std::min(tb, e - k * tb);
+        queues[x].push_back(it);
+      }
+      (void)p;
+    }
+    size_t depth = 0;
+    for (const auto& qx : queues) depth = std::max(depth, qx.size());
+    std::vector<ExtendItem> items(depth * kXcds);
+    for (size_t i = 0; i < depth; ++i)
+      for (int x = 0; x < kXcds; ++x) {
+        ExtendItem it = {0, 0, 0, 0};  // ntok == 0: an empty slot the kernel skips
+        if (i < queues[x].size()) it = queues[x][i];
+        items[i * kXcds + x] = it;
+      }
+    while (!items.empty() && items.back().ntok == 0) items.pop_back();
     n_items = (int64_t)items.size();
     if (build_blob) {
       items_bytes.resize(items.size() * sizeof(ExtendItem));
-      for (size_t i = 0; i < items.size(); ++i)
-        memcpy(items_bytes.data() + i * sizeof(ExtendItem), &items[i].it, sizeof(ExtendItem));
+      if (!items.empty()) memcpy(items_bytes.data(), items.data(), items_bytes.size());
     }
   } else {  // decode
     int64_t chunk = 0;

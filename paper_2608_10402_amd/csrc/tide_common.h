@@ -11,6 +11,7 @@ constexpr int kMaxGroup = 16;     // largest supported Hq / Hkv
 constexpr int kExtendKeyTile = 64;  // keys per extend-kernel iteration (4 pages)
 constexpr int kDecodeStep = 32;   // keys per decode-kernel iteration (2 pages)
 constexpr int kWsAlign = 256;
+constexpr int kXcds = 8;          // MI355X: 8 accelerator dies, one L2 each
 
 // One task as the kernels see it.  `row_start` indexes the packed token rows of Q/O
 // (extend, prefill) or the task itself (decode); tokens at positions
