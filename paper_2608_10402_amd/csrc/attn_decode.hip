@@ -9,11 +9,14 @@
 //     K/V load; they are the columns of v_mfma_f32_16x16x32_bf16 (G <= 16), so the
 //     contraction costs a few MFMA issues per 2 KB loaded and no VALU dot products.
 //   * Operands go straight from HBM into MFMA registers (no LDS): for S^T = K.Q^T a lane
-//     loads 16 contiguous bytes of one key row; for O^T += V^T.P^T it loads 16 bytes of
-//     a transposed V page (8 consecutive token slots of one head-dim entry).  Key rows
-//     are assigned so that each lane's probabilities are those 8 slots, so P never moves
-//     between lanes.
-//   * The next 32-key step is loaded while the current one is computed.
+//     loads 16 contiguous bytes of one key row; for O^T += V^T.P^T it loads two 8-byte
+//     pieces of transposed V pages (4 consecutive token slots of one head-dim entry in
+//     each page).  The S^T rows of page t are its token slots, so each lane's
+//     probabilities are exactly those slots and P never moves between lanes.
+//   * Every load instruction reads one page: the page block is a scalar base, lanes add
+//     a fixed offset.  Page ids arrive 64 at a time (one vector load, then readlane).
+//   * Two register buffers in ping-pong keep the next 32-key step in flight; at most
+//     256 registers so two waves share each SIMD.
 //   * Partial (o, m, l) per split go to the workspace; a second small kernel merges them.
 #include "kernels.h"
 #include "tide_device.h"
@@ -23,67 +26,54 @@ namespace kern {
 
 constexpr int kWavesPerBlock = 4;
 
+// One 32-key step (pages p0 = keys k..k+15 and p1 = k+16..k+31) in registers.
+//   k[t][c]: S^T operand for page t, head-dim chunk c (MFMA row = token slot)
+//   v[t][h]: V^T operand halves for head-dim tile t: slots 4*grp..4*grp+3 of page h
 template <int D>
 struct DecodeRegs {
-  u32x4 k[2][D / 32];  // two 16-key S tiles x head-dim chunks of 32
-  u32x4 v[D / 16];     // V^T operands, one per 16-row head-dim tile
+  u32x4 k[2][D / 32];
+  uint2 v[D / 16][2];
 };
 
+// Buffer resource of one (page, kv head) block: base in SGPRs, range = the block, so each
+// load is a 32-bit lane offset plus an immediate (raw buffer, gfx9 descriptor format).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t block_rsrc(const uint8_t* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), 0, bytes, 0x00020000);
+}
+
+// Loads of one step.  Every instruction reads a single page block.
 template <int D>
-__device__ __forceinline__ void load_step(DecodeRegs<D>& r, const DecodeArgs& a,
-                                          const int32_t* bt_row, int npages, int kv_len,
-                                          int kv_head, int k, int lane) {
-  const int lp0 = k / kPage;
-  int64_t base[2];
+__device__ __forceinline__ void load_step(DecodeRegs<D>& r, __amdgpu_buffer_rsrc_t k0,
+                                          __amdgpu_buffer_rsrc_t k1, __amdgpu_buffer_rsrc_t v0,
+                                          __amdgpu_buffer_rsrc_t v1, uint32_t k_off,
+                                          uint32_t v_off) {
 #pragma unroll
-  for (int pi = 0; pi < 2; ++pi) {
-    const int lp = lp0 + pi;
-    int64_t b = -1;
-    if (lp < npages) {
-      const int32_t p = bt_row[lp];
-      if (p >= 0 && p < a.num_pages) {
-        b = ((int64_t)p * a.num_kv_heads + kv_head) * (int64_t)(kPage * D);
-      } else if (lane == 0) {
-        atomicOr(a.error_flags, 1);
-      }
-    }
-    base[pi] = b;
+  for (int c = 0; c < D / 32; ++c) {
+    r.k[0][c] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(k0, k_off + 64 * c, 0, 0));
+    r.k[1][c] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(k1, k_off + 64 * c, 0, 0));
   }
-  const int row = lane & 15, grp = lane >> 4;
-  // K rows: S tile t, MFMA row `row` holds key 8*(row/4) + 4*t + row%4 of the 32-key step
-#pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int key = 8 * (row >> 2) + 4 * t + (row & 3);
-    const int64_t b = base[key >> 4];
-#pragma unroll
-    for (int c = 0; c < D / 32; ++c)
-      r.k[t][c] = b >= 0 ? load_u32x4(a.k_pool + b + (key & 15) * D + 32 * c + 8 * grp)
-                         : zero_u32x4();
-  }
-  // V^T: lane group grp holds keys 8*grp .. 8*grp+7 = page grp/2, slots 8*(grp&1) ..
-  const int64_t vb = base[grp >> 1];
-  const int slot0 = 8 * (grp & 1);
-  const int nvalid = kv_len - (k + 8 * grp);
 #pragma unroll
   for (int t = 0; t < D / 16; ++t) {
-    u32x4 x = vb >= 0 ? load_u32x4(a.v_pool + vb + (16 * t + row) * kPage + slot0)
-                      : zero_u32x4();
-    if (nvalid < 8) {
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const uint32_t lo = (2 * w < nvalid) ? 0x0000FFFFu : 0u;
-        const uint32_t hi = (2 * w + 1 < nvalid) ? 0xFFFF0000u : 0u;
-        x[w] &= (lo | hi);
-      }
-    }
-    r.v[t] = x;
+    r.v[t][0] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(v0, v_off + 512 * t, 0, 0));
+    r.v[t][1] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(v1, v_off + 512 * t, 0, 0));
   }
 }
 
+// Keep only the first n (0..4) bf16 elements of an 8-byte V^T piece.
+__device__ __forceinline__ uint2 keep_first4(uint2 x, int n) {
+  uint2 r;
+  r.x = x.x & ((n > 0 ? 0x0000FFFFu : 0u) | (n > 1 ? 0xFFFF0000u : 0u));
+  r.y = x.y & ((n > 2 ? 0x0000FFFFu : 0u) | (n > 3 ? 0xFFFF0000u : 0u));
+  return r;
+}
+
 template <int D>
-__global__ __launch_bounds__(kWavesPerBlock * 64) void decode_split_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kWavesPerBlock * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void decode_split_kernel(DecodeArgs a) {
   const int lane = threadIdx.x & 63;
-  const int item_id = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+  // the wave index is uniform across the wave: say so, so the item and every address
+  // derived from it stay scalar
+  const int item_id = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (item_id >= a.num_items) return;  // whole wave exits; no block-level barrier below
   const DecodeItem it = a.items[item_id];
   const TaskDesc td = a.tasks[it.task];
@@ -92,6 +82,9 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_split_kernel(Decod
   const int32_t* bt_row = a.block_table + (int64_t)it.task * a.bt_stride;
   const int G = a.group;
   const int col = lane & 15, grp = lane >> 4;
+  const uint8_t* kpool = reinterpret_cast<const uint8_t*>(a.k_pool);
+  const uint8_t* vpool = reinterpret_cast<const uint8_t*>(a.v_pool);
+  constexpr int64_t kBlk = (int64_t)kPage * D * 2;  // bytes of one (page, kv head) block
 
   // Q^T operand: column col = query head kv_head*G + col (zero when col >= G)
   bf16x8 qf[D / 32];
@@ -102,18 +95,40 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_split_kernel(Decod
 
   const int kbeg = it.k_begin;
   const int kend = min(kv_len, kbeg + a.chunk);
+  const uint32_t k_off = (uint32_t)(col * D * 2 + 16 * grp);       // token slot `col`
+  const uint32_t v_off = (uint32_t)(col * kPage * 2 + 8 * grp);    // head-dim row `col`
+
+  // Page ids of this split, 64 at a time: lane i holds logical page lp0 + i.
+  int lp_batch = -1;
+  int32_t pid = 0;
+  bool flag_error = false;  // an invalid page id was seen (reported once, at the end)
+  auto page_block = [&](int lp) -> int64_t {
+    if (lp - lp_batch >= 64 || lp_batch < 0) {
+      lp_batch = lp;
+      const int mine = lp + lane;
+      pid = mine < npages ? bt_row[mine] : 0;
+    }
+    const int32_t p = __builtin_amdgcn_readlane(pid, lp - lp_batch);
+    const bool bad = p < 0 || p >= a.num_pages || lp >= npages;
+    // pages past the context (and invalid ids) read page 0: masked / zeroed below
+    const int64_t blk = ((int64_t)(bad ? 0 : p) * a.num_kv_heads + it.kv_head) * kBlk;
+    if (bad && lp < npages) flag_error = true;
+    return blk;
+  };
+  auto load = [&](DecodeRegs<D>& r, int k) {
+    const int64_t b0 = page_block(k / kPage), b1 = page_block(k / kPage + 1);
+    load_step<D>(r, block_rsrc(kpool + b0, (int)kBlk), block_rsrc(kpool + b1, (int)kBlk),
+                 block_rsrc(vpool + b0, (int)kBlk), block_rsrc(vpool + b1, (int)kBlk), k_off,
+                 v_off);
+  };
 
   f32x4 o[D / 16];
 #pragma unroll
   for (int t = 0; t < D / 16; ++t) o[t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   float m_ref = kNoMax, l_part = 0.0f, l_exact = 0.0f;
 
-  DecodeRegs<D> cur, nxt;
-  load_step<D>(cur, a, bt_row, npages, kv_len, it.kv_head, kbeg, lane);
-  for (int k = kbeg; k < kend; k += kDecodeStep) {
-    const bool more = k + kDecodeStep < kend;
-    if (more) load_step<D>(nxt, a, bt_row, npages, kv_len, it.kv_head, k + kDecodeStep, lane);
-
+  auto compute = [&](DecodeRegs<D>& cur, int k) {
+    // S^T for page t: s[t][e] is key k + 16*t + 4*grp + e of query head `col`
     f32x4 s[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -121,17 +136,24 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_split_kernel(Decod
 #pragma unroll
       for (int c = 0; c < D / 32; ++c) s[t] = mfma16(as_bf16x8(cur.k[t][c]), qf[c], s[t]);
     }
-    // s[t][e] is key k + 8*grp + 4*t + e of query head `col`
+    const bool tail = k + 2 * kPage > kv_len;
     float mt = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         float x = s[t][e] * a.scale_log2;
-        x = (k + 8 * grp + 4 * t + e < kv_len) ? x : -INFINITY;
+        if (tail) x = (k + 16 * t + 4 * grp + e < kv_len) ? x : -INFINITY;
         s[t][e] = x;
         mt = fmaxf(mt, x);
       }
+    if (tail) {  // V slots past the context must not reach the MFMA (NaN * 0 = NaN)
+#pragma unroll
+      for (int t = 0; t < D / 16; ++t)
+#pragma unroll
+        for (int hp = 0; hp < 2; ++hp)
+          cur.v[t][hp] = keep_first4(cur.v[t][hp], kv_len - (k + 16 * hp + 4 * grp));
+    }
     mt = fmaxf(mt, xor_shfl(mt, 16));
     mt = fmaxf(mt, xor_shfl(mt, 32));
     if (__any(mt > m_ref + kRescaleSlack)) {
@@ -143,6 +165,7 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_split_kernel(Decod
       for (int t = 0; t < D / 16; ++t) o[t] *= alpha;
       m_ref = m_new;
     }
+    // P^T operand: slots 0..3 = page 0 keys 4*grp.., slots 4..7 = page 1 keys 4*grp..
     u32x4 w;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -156,10 +179,24 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_split_kernel(Decod
       }
     const bf16x8 pb = as_bf16x8(w);
 #pragma unroll
-    for (int t = 0; t < D / 16; ++t) o[t] = mfma16(as_bf16x8(cur.v[t]), pb, o[t]);
-    if (more) cur = nxt;
+    for (int t = 0; t < D / 16; ++t) {
+      const u32x4 vv = {cur.v[t][0].x, cur.v[t][0].y, cur.v[t][1].x, cur.v[t][1].y};
+      o[t] = mfma16(as_bf16x8(vv), pb, o[t]);
+    }
+  };
+
+  // Two register buffers in ping-pong: the next step is in flight while one is used.
+  DecodeRegs<D> ra, rb;
+  load(ra, kbeg);
+  for (int k = kbeg; k < kend; k += 2 * kDecodeStep) {
+    if (k + kDecodeStep < kend) load(rb, k + kDecodeStep);
+    compute(ra, k);
+    if (k + kDecodeStep >= kend) break;
+    if (k + 2 * kDecodeStep < kend) load(ra, k + 2 * kDecodeStep);
+    compute(rb, k + kDecodeStep);
   }
 
+  if (flag_error && lane == 0) atomicOr(a.error_flags, 1);
   float l_tot = l_part + xor_shfl(l_part, 16);
   l_tot += xor_shfl(l_tot, 32);
   float l_ex = l_exact + xor_shfl(l_exact, 16);
