@@ -1,20 +1,28 @@
 #!/usr/bin/env python3
 """Benchmark of the paged-KV resume-attention hot path on one MI355X.
 
-One step is one pass over every stage of the path for the agent-resume workload
-(64 tasks, 28 query / 4 KV heads, head_dim 128, page 16, prefixes U{2048..16384},
-observations log-uniform 64..2048, fragmented page placement):
+One step is one pass over every stage of the path for the chosen workload (default
+agent_resume_7b: 64 tasks, 28 query / 4 KV heads, head_dim 128, page 16, prefixes
+U{2048..16384}, observations log-uniform 64..2048, fragmented page placement):
+
+  extend workloads (agent_resume_7b, multimodal_resume, tiny_extend)
     1. KV-append of the new observation tokens           (tide_kv_append)
     2. extend attention over the retained prefix         (tide_extend_attn)
     3. decode attention of one token per task (split-K)  (tide_decode_attn)
-    4. the recompute a cache miss forces: KV-append of the whole history, then
-       full causal re-prefill attention                   (tide_kv_append, tide_full_prefill_attn)
+    4. with --reprefill 1, the recompute a cache miss forces: KV-append of the whole
+       history, then full causal re-prefill attention     (tide_kv_append, tide_full_prefill_attn)
+  resumed_decode
+    1. KV-append of each task's decoded token, 2. split-K decode over its context
+  long_horizon
+    1. KV-append of the new tokens, 2. extend, 3. eight rounds of (append one token, decode)
+
 Inputs are resident in HBM before timing starts; every kernel call is timed with HIP
 events on the stream it is launched on.
 
-Printed: one JSON line.  `value` is extend-attention throughput in TFLOP/s over the
-unmasked (query, key) pairs (4*d flops per pair and query head).  The line also
-carries the decode GB/s, the speedup of extend over re-prefill, the roofline of the
+Printed: one JSON line.  For extend workloads `value` is extend-attention throughput in
+TFLOP/s over the unmasked (query, key) pairs (4*d flops per pair and query head); for
+resumed_decode it is decode-attention GB/s of algorithmic bytes.  The line also carries
+the other stages' rates, the speedup of extend over re-prefill, the roofline of the
 dominant kernel, and the fp64 oracle timed on a bounded sample on the host.
 """
 from __future__ import annotations
@@ -35,8 +43,12 @@ sys.path.insert(0, ROOT)
 METRIC = "extend-attn TFLOP/s (% bf16 peak); decode-attn GB/s (% HBM); speedup vs re-prefill"
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
-PROFILE_SUMMARY = os.path.join(ROOT, "profiles", "attn_extend_agent_resume_7b_counters.txt")
-EXTEND_SOURCE = os.path.join(ROOT, "paper_2608_10402_amd", "csrc", "attn_extend.hip")
+# rocprofv3 counter summaries (copy-calibrated FETCH_SIZE + WRITE_SIZE per launch), keyed by
+# (workload, dominant kernel); each records the hash of the kernel source it was taken on.
+PROFILE_SUMMARIES = {
+    ("agent_resume_7b", "extend"): ("attn_extend_agent_resume_7b_counters.txt", "attn_extend.hip"),
+    ("resumed_decode", "decode"): ("decode_split_resumed_decode_counters.txt", "attn_decode.hip"),
+}
 
 
 def parse_args():
@@ -78,17 +90,22 @@ def append_bytes(wl, tokens: int) -> float:
     return float(tokens) * s.num_kv_heads * s.head_dim * 2 * 2 * 2  # K+V, read + write
 
 
-def counter_traffic():
-    """HBM bytes per extend launch from the committed rocprofv3 counter summary, or None
-    when the kernel source changed since the counters were taken."""
-    if not os.path.exists(PROFILE_SUMMARY):
+def counter_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter
+    summary, or None when there is none or the kernel source changed since."""
+    entry = PROFILE_SUMMARIES.get((workload, kernel))
+    if entry is None:
         return None
-    text = open(PROFILE_SUMMARY).read()
+    path = os.path.join(ROOT, "profiles", entry[0])
+    src = os.path.join(ROOT, "paper_2608_10402_amd", "csrc", entry[1])
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
     m_hash = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
     m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not m_hash or not m_bytes:
         return None
-    cur = hashlib.sha256(open(EXTEND_SOURCE, "rb").read()).hexdigest()
+    cur = hashlib.sha256(open(src, "rb").read()).hexdigest()
     return float(m_bytes.group(1)) if cur == m_hash.group(1) else None
 
 
@@ -290,7 +307,7 @@ def main():
     primary = "extend" if "extend" in rooflines else "decode"
     roofline = dict(rooflines[primary])
     roofline["kernel"] = "extend_attn_kernel" if primary == "extend" else "decode_split_kernel"
-    roofline["traffic"] = counter_traffic() if (primary == "extend" and s.key == "agent_resume_7b") else None
+    roofline["traffic"] = counter_traffic(s.key, primary)
 
     cpu = None
     if args.cpu_seconds > 0 and "extend" in ms:
