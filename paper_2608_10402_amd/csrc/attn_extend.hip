@@ -6,15 +6,25 @@
 // Method: FlashAttention-2-style streaming softmax (Dao 2023; online softmax of Milakov
 // & Gimelshein 2018) over K/V gathered page by page (PagedAttention, Kwon et al. 2023),
 // laid out for CDNA4:
-//   * A workgroup (4 waves) owns one (task, kv head, block of tokens) item.  Its 128
+//   * A workgroup of 8 waves owns one (task, kv head, block of tokens) item.  Its 256
 //     query rows are the (token, head) pairs of the block for every query head of the kv
-//     head, so each K/V tile in LDS serves all G grouped heads at once.
-//   * K/V tiles of 64 keys (4 pages) go from HBM straight into LDS with
-//     global_load_lds_dwordx4 (no staging registers); wave w fetches page w of the tile.
-//     Two LDS buffers: the next tile streams in while the current one is used.
-//   * Each wave computes S^T = K.Q^T for its 32 rows with v_mfma_f32_32x32x16_bf16:
-//     keys are the MFMA rows, queries the columns, so every lane owns one query row and
-//     its softmax statistics need one cross-lane exchange (lanes l and l^32).
+//     head, so each K/V tile in LDS serves all G grouped heads at once.  One workgroup
+//     fills a CU: two waves per SIMD.
+//   * Two waves per SIMD (waves w and w+4) share the SIMD in a fixed rotation.  Every
+//     wave alternates a matrix phase (P.V of the previous tile, then S = K.Q^T of the
+//     current one: 32 MFMAs) and vector work (mask, running max, exp2, bf16 packing,
+//     row sums).  Workgroup barriers cut each tile into three slots: in the first two,
+//     one group's MFMAs overlap the other group's VALU work; in the third, no MFMA runs
+//     and both groups evaluate their exponentials, because v_exp_f32 does not overlap
+//     MFMAs on the same SIMD.
+//   * K/V tiles of 64 keys (4 pages) go from HBM straight into LDS with buffer loads
+//     that write LDS (no staging registers).  Four LDS buffers: in its vector phase of
+//     tile i every wave streams one page of tile i+3 (waves 0-3 the K pages, waves 4-7
+//     the V^T pages), so a tile has about four phases to arrive.  Page ids are read
+//     with scalar loads.
+//   * S^T = K.Q^T per wave with v_mfma_f32_32x32x16_bf16: keys are the MFMA rows,
+//     queries the columns, so every lane owns one query row and its softmax statistics
+//     need one exchange between lanes l and l^32 (v_permlane32_swap, a VALU op).
 //   * Key rows are read in the perm32 order, which leaves each lane holding runs of 8
 //     consecutive keys: the probabilities convert straight into the B operand of the
 //     O^T += V^T.P^T MFMA with no shuffle.  V pages are stored transposed in the pool
@@ -24,18 +34,18 @@
 //   * Scores stay raw until one FMA applies sm_scale*log2(e) and subtracts the running
 //     max before v_exp_f32.  The running max is only raised when a tile exceeds it by
 //     more than kRescaleSlack, so the O rescale is skipped on almost every tile.
-//   * Causal masking is applied only on tiles that cross the diagonal.  V slots at or
-//     beyond the task's length (the last tile) are zeroed in LDS before use, so NaN/Inf
-//     garbage in unused pool slots can never reach the output.
-//   * At most 256 registers per lane, so two workgroups share a CU and one's softmax
-//     overlaps the other's matrix work.
+//   * Causal masking is applied only on tiles that cross the diagonal.  On the last
+//     tile, V operands of key slots at or beyond the task's length are zeroed in
+//     registers, so NaN/Inf garbage in unused pool slots can never reach the output.
+#include <type_traits>
+
 #include "kernels.h"
 #include "tide_device.h"
 
 namespace tide {
 namespace kern {
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;  // two groups of four, one phase apart
 constexpr int kThreads = kWaves * 64;
 
 template <int D>
@@ -47,8 +57,25 @@ struct ES {
   static constexpr int kTileBytes = 4 * kPageBytes;  // 64 keys
   static constexpr int kDma = kPageBytes / 1024;     // 1 KB wave transfers per page
   static constexpr int kRowsPerDma = 1024 / kRowBytes;
+  static constexpr int kLoads = 2 * kDma;            // vector-memory ops per streamed tile
   static_assert(kDma >= 1 && kRowsPerDma * kRowBytes == 1024, "page split");
 };
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef const __attribute__((address_space(4))) int32_t const_i32;
+
+// Block-table word `idx` of a row, read through the constant address space: the table is
+// read-only during the kernel, so a wave-uniform index becomes a scalar load.
+__device__ __forceinline__ int32_t load_page_id(const int32_t* row, int idx) {
+  return ((const_i32*)row)[idx];
+}
+
+// 16 bytes per lane from `page` (a buffer of `bytes` bytes; reads past it return 0) at
+// byte offset `voff`, written by the buffer unit straight into LDS at lds + 16 * lane.
+__device__ __forceinline__ void dma16(const uint8_t* page, int bytes, uint32_t voff, uint8_t* lds) {
+  const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(page), 0, bytes, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)lds, 16, voff, 0, 0, 0);
+}
 
 // Swizzled position of granule g in K row r.
 template <int D>
@@ -60,70 +87,45 @@ __device__ __forceinline__ int kswz(int r, int g) {
 // so the halves of rows with bit 3 set are swapped.
 __device__ __forceinline__ int vswz(int d, int hh) { return hh ^ ((d >> 3) & 1); }
 
-__device__ __forceinline__ void wait_all_vmem() {
-  // s_waitcnt vmcnt(0) (gfx9 encoding: expcnt and lgkmcnt left at their maxima)
-  __builtin_amdgcn_s_waitcnt(0x0F70);
+// s_waitcnt vmcnt(N) (gfx9 encoding; expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
 
-template <int D>
-struct Ctx {
-  const uint8_t* k_pool;
-  const uint8_t* v_pool;
-  int32_t* error_flags;
-  int64_t num_pages;
-  int num_kv_heads;
-  const int32_t* bt_row;
-  int npages;
-  int seq_len;
-  int kv_head;
-  int wave;
-  int lane;
-  uint32_t k_dma_off[ES<D>::kDma];  // this lane's source offset inside a K page, per transfer
-  uint32_t v_dma_off[ES<D>::kDma];  // same for the V^T page
+// Workgroup barrier between phases, with no memory fence: LDS tiles are published by
+// each wave's own vmcnt wait before it, and outstanding prefetches must stay in flight.
+// The scheduling barriers keep every instruction in the phase it was written in (the
+// compiler would otherwise move MFMAs, which touch no memory, across s_barrier).
+__device__ __forceinline__ void phase_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
 
-  // Block-table word of this wave's page (page `wave`) of tile `tile`, loaded as a vector
-  // value: it is issued one tile ahead and only read after the next vmcnt(0), so the
-  // memory round trip overlaps a whole tile of compute instead of stalling the issue.
-  __device__ __forceinline__ int32_t fetch_page(int tile) const {
-    const int lp = tile * 4 + wave;
-    return lp < npages ? bt_row[lp] : 0;
-  }
+// Values of lanes l and l^32 side by side.  v_permlane32_swap trades lanes 32-63 of its
+// first operand with lanes 0-31 of its second; starting from two copies of v, the first
+// ends up holding the low half twice and the second the high half twice.  It is issued
+// by hand because the compiler folds the intrinsic's second result into its first.  The
+// s_nop provides the wait states this instruction needs after a VALU write of its inputs.
+__device__ __forceinline__ void lane_pair(float v, float& x, float& y) {
+  uint32_t lo = __builtin_bit_cast(uint32_t, v), hi = lo;
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(lo), "+v"(hi));
+  x = __builtin_bit_cast(float, lo);
+  y = __builtin_bit_cast(float, hi);
+}
 
-  // Issue this wave's share of a tile, whose page id `word` came from fetch_page().
-  __device__ __forceinline__ void issue_tile(int32_t word, uint8_t* kb, uint8_t* vb) const {
-    using S = ES<D>;
-    // One word for the whole wave: kept scalar, as is all the address math below.
-    const int32_t p = __builtin_amdgcn_readfirstlane(word);
-    const bool bad = p < 0 || p >= num_pages;
-    const int64_t page = bad ? 0 : p;
-    if (bad && lane == 0) atomicOr(error_flags, 1);
-    // Pages past the sequence (and invalid ids) are read from page 0, which always
-    // exists; their keys are masked and their V slots zeroed before use.
-    const int64_t blk = (page * num_kv_heads + kv_head) * (int64_t)S::kPageBytes;
-    const uint8_t* kg = k_pool + blk;
-    const uint8_t* vg = v_pool + blk;
-    uint8_t* kd = kb + wave * S::kPageBytes;
-    uint8_t* vd = vb + wave * S::kPageBytes;
-#pragma unroll
-    for (int i = 0; i < S::kDma; ++i) {
-      __builtin_amdgcn_global_load_lds(kg + k_dma_off[i], kd + i * 1024, 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vg + v_dma_off[i], vd + i * 1024, 16, 0, 0);
-    }
-  }
-};
+__device__ __forceinline__ float pair_max(float v) {
+  float x, y;
+  lane_pair(v, x, y);
+  return fmaxf(x, y);
+}
 
-// Zero the V^T slots of keys >= seq_len in a tile (only the last tile of an item).
-template <int D>
-__device__ __forceinline__ void zero_tail(uint8_t* vb, int k0, int seq_len, int tid) {
-  using S = ES<D>;
-  for (int row = tid; row < 4 * D; row += kThreads) {
-    const int pi = row / D, d = row % D;
-    const int nvalid = seq_len - (k0 + pi * kPage);
-    if (nvalid >= kPage) continue;
-    uint8_t* r = vb + pi * S::kPageBytes + d * (kPage * 2);
-    for (int s = nvalid < 0 ? 0 : nvalid; s < kPage; ++s)
-      *reinterpret_cast<uint16_t*>(r + vswz(d, s >> 3) * 16 + (s & 7) * 2) = 0;
-  }
+__device__ __forceinline__ float pair_sum(float v) {
+  float x, y;
+  lane_pair(v, x, y);
+  return x + y;
 }
 
 // kLse: also keep the exact fp32 sum of the probabilities, so the returned log-sum-exp is
@@ -135,14 +137,19 @@ void extend_attn_kernel(ExtendArgs a) {
   using S = ES<D>;
   constexpr int kDC = D / 16;  // 16-wide head-dim chunks of QK^T
   constexpr int kDT = D / 32;  // 32-row head-dim tiles of O^T
-  __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[S::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t k_lds1[S::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t v_lds0[S::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t v_lds1[S::kTileBytes];
+  // Tile buffers: K at offset 0, V^T at kTileBytes.  One array per buffer lets the
+  // compiler track in-flight LDS writes per buffer, so reading one buffer never waits
+  // for the prefetch into another.
+  __shared__ __attribute__((aligned(1024))) uint8_t kv_lds0[2 * S::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t kv_lds1[2 * S::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t kv_lds2[2 * S::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t kv_lds3[2 * S::kTileBytes];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool v_half = wave >= 4;  // waves 4-7: V^T pages, one phase behind; 0-3: K pages
+  const int pw = wave & 3;        // page of every tile this wave fetches
   const int q = lane & 31, h = lane >> 5;
 
   const ExtendItem it = a.items[blockIdx.x];
@@ -151,33 +158,45 @@ void extend_attn_kernel(ExtendArgs a) {
   const int P = td.prefix;
   const int seq_len = td.prefix + td.extend;
   const int G = a.group;
+  const int npages = (seq_len + kPage - 1) / kPage;
+  const int kend = P + it.tok0 + it.ntok;     // keys needed by the last row
+  const int ntiles = (kend + 63) / 64;
+  const int n_full = (P + it.tok0 + 1) / 64;  // tiles every row sees completely
 
-  Ctx<D> c;
-  c.k_pool = reinterpret_cast<const uint8_t*>(a.k_pool);
-  c.v_pool = reinterpret_cast<const uint8_t*>(a.v_pool);
-  c.error_flags = a.error_flags;
-  c.num_pages = a.num_pages;
-  c.num_kv_heads = a.num_kv_heads;
-  c.bt_row = a.block_table + (int64_t)it.task * a.bt_stride;
-  c.npages = (seq_len + kPage - 1) / kPage;
-  c.seq_len = seq_len;
-  c.kv_head = it.kv_head;
-  c.wave = wave;
-  c.lane = lane;
+  // ---- K/V streaming: waves 0-3 fetch the K pages, waves 4-7 the V^T pages ---------
+  const int32_t* bt = a.block_table + (int64_t)it.task * a.bt_stride;
+  const uint8_t* src_pool = reinterpret_cast<const uint8_t*>(v_half ? a.v_pool : a.k_pool);
+  const int lds_half = v_half ? S::kTileBytes : 0;  // V^T lives after K in each buffer
+  uint32_t src_off[S::kDma];  // this lane's byte offset inside a K or V^T page, per transfer
 #pragma unroll
   for (int i = 0; i < S::kDma; ++i) {
-    const int r = i * S::kRowsPerDma + lane / S::kNG;  // row inside the page (== tile row mod 16)
-    const int g = kswz<D>(r, lane % S::kNG);
-    c.k_dma_off[i] = (uint32_t)(r * S::kRowBytes + g * 16);
-    const int d = i * 32 + lane / 2;  // V^T row (head-dim entry) this lane's granule lands in
-    c.v_dma_off[i] = (uint32_t)(d * (kPage * 2) + vswz(d, lane & 1) * 16);
+    const int r = i * S::kRowsPerDma + lane / S::kNG;  // K row inside the page
+    const int d = i * 32 + lane / 2;                   // V^T row (head-dim entry)
+    src_off[i] = v_half ? (uint32_t)(d * (kPage * 2) + vswz(d, lane & 1) * 16)
+                        : (uint32_t)(r * S::kRowBytes + kswz<D>(r, lane % S::kNG) * 16);
   }
+  bool bad_page = false;
+  // Page id of this wave's page of `tile` (a scalar load); pages past the sequence are
+  // read from page 0, which always exists: their keys are masked, their V zeroed.
+  auto page_word = [&](int tile) -> int32_t {
+    const int lp = tile * 4 + pw;
+    return lp < npages ? load_page_id(bt, lp) : 0;
+  };
+  // Every step issues the same number of loads on every wave, so the vmcnt waits below
+  // hold on every path; a tile past the item (live == false) is read through a
+  // zero-length buffer, which returns zeros without touching memory.
+  auto stream_tile = [&](int32_t word, uint8_t* kv, bool live) {
+    const bool bad = live && (word < 0 || (int64_t)word >= a.num_pages);
+    bad_page |= bad;
+    const int64_t blk = ((bad ? 0 : (int64_t)word) * a.num_kv_heads + it.kv_head) *
+                        (int64_t)S::kPageBytes;
+    const int bytes = live ? S::kPageBytes : 0;
+#pragma unroll
+    for (int i = 0; i < S::kDma; ++i)
+      dma16(src_pool + blk, bytes, src_off[i], kv + lds_half + pw * S::kPageBytes + i * 1024);
+  };
 
-  // start streaming tile 0 before anything else
-  c.issue_tile(c.fetch_page(0), k_lds0, v_lds0);
-  int32_t next_page = c.fetch_page(1);  // page id of the tile the next step streams in
-
-  // this lane's query row: (token tk of the block, head j of the group)
+  // ---- this lane's query row: (token tk of the block, head j of the group) -----------
   const int r = wave * 32 + q;
   const int tk = r / G, j = r - (r / G) * G;
   const bool row_valid = tk < it.ntok;
@@ -189,16 +208,23 @@ void extend_attn_kernel(ExtendArgs a) {
   for (int cc = 0; cc < kDC; ++cc)
     qf[cc] = as_bf16x8(row_valid ? load_u32x4(a.q + qrow * D + 16 * cc + 8 * h) : zero_u32x4());
 
+  // ---- prologue: tiles 0..2 in flight, tile 0 landed, then the phase offset ---------
+  stream_tile(page_word(0), kv_lds0, true);
+  __builtin_amdgcn_sched_barrier(0);  // keep the issue order the waits below count on
+  stream_tile(page_word(1), kv_lds1, ntiles > 1);
+  __builtin_amdgcn_sched_barrier(0);
+  stream_tile(page_word(2), kv_lds2, ntiles > 2);
+  int32_t next_word = page_word(3);  // page id of the next tile to stream
+  wait_vmem<2 * S::kDma>();          // tile 0 (and the query rows) landed
+  phase_barrier();
+  if (v_half) phase_barrier();  // waves 4-7 start one phase behind
+
   // per-lane LDS byte offsets of the MFMA operands
   const int krow = perm32(q);
   int k_rd[kDC];
 #pragma unroll
   for (int cc = 0; cc < kDC; ++cc) k_rd[cc] = krow * S::kRowBytes + kswz<D>(krow, 2 * cc + h) * 16;
   const int v_rd = krow * (kPage * 2) + vswz(krow, h) * 16;
-
-  const int kend = P + it.tok0 + it.ntok;           // keys needed by the last row
-  const int ntiles = (kend + 63) / 64;
-  const int n_full = (P + it.tok0 + 1) / 64;        // tiles every row sees completely
   const float csc = a.scale_log2;
 
   f32x16 o[kDT];
@@ -207,33 +233,64 @@ void extend_attn_kernel(ExtendArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[t][e] = 0.0f;
   float m_ref = kNoMax, l_part = 0.0f, l_exact = 0.0f;
+  f32x16 s[2];
+  u32x4 pb[4];  // bf16 probabilities of the last softmaxed tile, one 16-key chunk each
 
-  auto compute = [&](const uint8_t* kb, const uint8_t* vb, int tile) {
-    f32x16 s[2];
-    {
-      u32x4 kf[2][kDC];
+  // O^T += V^T.P^T for `tile`, V^T in vb.  With kTail, the V slots of keys at or beyond
+  // seq_len are zeroed in registers (0 * NaN would otherwise poison O); only an item's
+  // last tile can hold such keys.
+  auto pv = [&](const uint8_t* vb, int tile, auto tail_tag) {
+    constexpr bool kTail = decltype(tail_tag)::value;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      u32x4 msk = {~0u, ~0u, ~0u, ~0u};
+      if (kTail) {
+        const int nv = seq_len - (tile * 64 + 16 * c + 8 * h);  // valid keys of this lane's 8
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          msk[w] = (2 * w < nv ? 0x0000FFFFu : 0u) | (2 * w + 1 < nv ? 0xFFFF0000u : 0u);
+      }
+      const uint8_t* vp = vb + c * S::kPageBytes + v_rd;
+#pragma unroll
+      for (int t = 0; t < kDT; ++t) {
+        u32x4 vv = load_u32x4(vp + t * 1024);
+        if (kTail) vv &= msk;
+        o[t] = mfma32(as_bf16x8(vv), as_bf16x8(pb[c]), o[t]);
+      }
+    }
+  };
+
+  // S^T = K.Q^T for the tile held in kb.
+  auto qk = [&](const uint8_t* kb) {
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[st][e] = 0.0f;
+#pragma unroll
+    for (int cc = 0; cc < kDC; ++cc)
 #pragma unroll
       for (int st = 0; st < 2; ++st)
+        s[st] = mfma32(as_bf16x8(load_u32x4(kb + st * 32 * S::kRowBytes + k_rd[cc])), qf[cc], s[st]);
+  };
+
+  // Keep four operand reads in flight ahead of the MFMAs of a matrix phase with n of
+  // each: reads first, then MFMA/read pairs, then the last MFMAs.
+  auto pipeline = [](auto n_tag) {
+    constexpr int n = decltype(n_tag)::value;
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-        for (int cc = 0; cc < kDC; ++cc)
-          kf[st][cc] = load_u32x4(kb + st * 32 * S::kRowBytes + k_rd[cc]);
-#pragma unroll
-      for (int st = 0; st < 2; ++st) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) s[st][e] = 0.0f;
-#pragma unroll
-        for (int cc = 0; cc < kDC; ++cc) s[st] = mfma32(as_bf16x8(kf[st][cc]), qf[cc], s[st]);
-      }
-      // Keep kDC operand reads in flight ahead of the MFMAs: all reads of the first
-      // half, then MFMA/read pairs, then the last MFMAs.
-      __builtin_amdgcn_sched_group_barrier(0x100, kDC, 0);
-#pragma unroll
-      for (int i = 0; i < kDC; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, kDC, 0);
+    for (int i = 0; i < n - 4; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+  };
+
+  // The softmax of a tile, in three parts.  o1: causal mask, running max (and the rare
+  // rescale of O), then x = s * scale * log2(e) - max in place.  ex: 2^x in place
+  // (v_exp_f32, which does not overlap MFMAs on the same SIMD).  o2: bf16 packing into
+  // pb and the row sums.
+  auto softmax_o1 = [&](int tile) {
     if (tile >= n_full) {  // diagonal / tail tile: hide keys past this row's position
       const int kbase = tile * 64 + 8 * h;
 #pragma unroll
@@ -247,7 +304,7 @@ void extend_attn_kernel(ExtendArgs a) {
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int e = 0; e < 16; ++e) mt = fmaxf(mt, s[st][e]);
-    mt = fmaxf(mt, xor_shfl(mt, 32)) * csc;
+    mt = pair_max(mt) * csc;
     if (__any(mt > m_ref + kRescaleSlack)) {
       const float m_new = fmaxf(m_ref, mt);
       const float alpha = fast_exp2(m_ref - m_new);
@@ -260,50 +317,93 @@ void extend_attn_kernel(ExtendArgs a) {
       m_ref = m_new;
     }
     const float negm = -m_ref;
-    float lt = 0.0f, le = 0.0f;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        u32x4 w;
+      for (int e = 0; e < 16; ++e) s[st][e] = fmaf(s[st][e], csc, negm);
+  };
+  auto softmax_ex = [&]() {
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[st][e] = fast_exp2(s[st][e]);
+  };
+  auto softmax_o2 = [&]() {
+    float lt[4] = {0.0f, 0.0f, 0.0f, 0.0f}, le = 0.0f;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int m = 0; m < 2; ++m)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float p0 = fast_exp2(fmaf(s[st][8 * m + 2 * e], csc, negm));
-          const float p1 = fast_exp2(fmaf(s[st][8 * m + 2 * e + 1], csc, negm));
-          w[e] = pack_bf16x2(p0, p1);
-          lt = add_bf16x2(w[e], lt);
+          const float p0 = s[st][8 * m + 2 * e], p1 = s[st][8 * m + 2 * e + 1];
+          const uint32_t w = pack_bf16x2(p0, p1);
+          pb[2 * st + m][e] = w;
+          lt[e] = add_bf16x2(w, lt[e]);
           if (kLse) le += p0 + p1;
         }
-        const bf16x8 pb = as_bf16x8(w);
-        const uint8_t* vp = vb + (2 * st + m) * S::kPageBytes + v_rd;
-#pragma unroll
-        for (int t = 0; t < kDT; ++t)
-          o[t] = mfma32(as_bf16x8(load_u32x4(vp + t * 1024)), pb, o[t]);
-      }
-    l_part += lt;  // short dot2 chains per tile, IEEE adds across tiles
+    l_part += (lt[0] + lt[1]) + (lt[2] + lt[3]);  // short dot2 chains per tile
     if (kLse) l_exact += le;
   };
 
-  auto step = [&](int tile, uint8_t* kb, uint8_t* vb, uint8_t* kn, uint8_t* vn) {
-    wait_all_vmem();
-    __syncthreads();  // tile landed for every wave; the other buffer is free again
-    if ((tile + 1) * 64 > seq_len) {
-      zero_tail<D>(vb, tile * 64, seq_len, tid);
-      __syncthreads();
+  // One tile is a round of three slots, each closed by a workgroup barrier:
+  //   slot 1: waves 0-3 matrix phase (P.V of tile-1, S of tile)  | waves 4-7 o2 of tile-1
+  //   slot 2: waves 0-3 o1 of tile                              | waves 4-7 matrix phase
+  //   slot 3: waves 0-3 ex, o2 of tile                          | waves 4-7 o1, ex of tile
+  // Every wave runs the same code; only where its second barrier falls differs.  The
+  // exponentials of both groups meet in slot 3, where no MFMA runs, and the rest of the
+  // vector work overlaps the other group's MFMAs.  In o1 each wave also streams its page
+  // of tile+3 (waves 0-3 K, waves 4-7 V^T) into the buffer tile-1 has released, and at
+  // the end of the round waits until only its last two tiles are in flight, so tile+1
+  // is in LDS before the next round starts.
+  auto step = [&](int tile, uint8_t* kv, uint8_t* kv_prev) {
+    if (tile > 0) {
+      pv(kv_prev + S::kTileBytes, tile - 1, std::false_type());
+      qk(kv);
+      pipeline(std::integral_constant<int, 4 * kDT + 2 * kDC>());
+    } else {
+      qk(kv);
+      pipeline(std::integral_constant<int, 2 * kDC>());
     }
-    if (tile + 1 < ntiles) {
-      c.issue_tile(next_page, kn, vn);
-      next_page = c.fetch_page(tile + 2);
-    }
-    compute(kb, vb, tile);
+    phase_barrier();
+    stream_tile(next_word, kv_prev, tile + 3 < ntiles);
+    next_word = page_word(tile + 4);
+    softmax_o1(tile);
+    if (!v_half) phase_barrier();
+    softmax_ex();
+    if (v_half) phase_barrier();
+    softmax_o2();
+    wait_vmem<2 * S::kDma>();
+    phase_barrier();
   };
 
-  for (int tile = 0; tile < ntiles; tile += 2) {
-    step(tile, k_lds0, v_lds0, k_lds1, v_lds1);
-    if (tile + 1 < ntiles) step(tile + 1, k_lds1, v_lds1, k_lds0, v_lds0);
+  // Four steps per iteration with no conditions inside, so the compiler's view of the
+  // loads in flight matches the schedule; the last 0-3 tiles follow the loop.
+  int tile = 0;
+  for (; tile + 4 <= ntiles; tile += 4) {
+    step(tile, kv_lds0, kv_lds3);
+    step(tile + 1, kv_lds1, kv_lds0);
+    step(tile + 2, kv_lds2, kv_lds1);
+    step(tile + 3, kv_lds3, kv_lds2);
   }
+  if (tile < ntiles) {
+    step(tile, kv_lds0, kv_lds3);
+    if (tile + 1 < ntiles) {
+      step(tile + 1, kv_lds1, kv_lds0);
+      if (tile + 2 < ntiles) step(tile + 2, kv_lds2, kv_lds1);
+    }
+  }
+  switch ((ntiles - 1) & 3) {  // P.V of the last tile
+    case 0: pv(kv_lds0 + S::kTileBytes, ntiles - 1, std::true_type()); break;
+    case 1: pv(kv_lds1 + S::kTileBytes, ntiles - 1, std::true_type()); break;
+    case 2: pv(kv_lds2 + S::kTileBytes, ntiles - 1, std::true_type()); break;
+    default: pv(kv_lds3 + S::kTileBytes, ntiles - 1, std::true_type()); break;
+  }
+  if (!v_half) phase_barrier();  // balances the offset barrier of waves 4-7
+  wait_vmem<0>();  // no transfer into LDS may outlive the workgroup
 
-  const float l_tot = l_part + xor_shfl(l_part, 32);
+  if (bad_page && lane == 0) atomicOr(a.error_flags, 1);
+  const float l_tot = pair_sum(l_part);
   if (row_valid) {
     const float inv = 1.0f / l_tot;
     uint16_t* orow = a.out + qrow * D;
@@ -318,7 +418,7 @@ void extend_attn_kernel(ExtendArgs a) {
         store_u32x4(orow + 32 * t + 16 * half + 8 * h, w);
       }
     if (kLse) {
-      const float l_ex = l_exact + xor_shfl(l_exact, 32);
+      const float l_ex = pair_sum(l_exact);
       if (h == 0) a.lse[qrow] = (m_ref + __log2f(l_ex)) * kLn2;
     }
   }
