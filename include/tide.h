@@ -66,8 +66,9 @@
  * Calls enqueue work on `stream` and return without synchronizing (except under
  * TIDE_DEBUG_CHECKS=1).  Device faults surface at the caller's next synchronization.
  * No C++ exception or abort crosses this interface.  The library never allocates
- * device memory; it keeps a small pinned host staging ring (created lazily, released
- * by tide_shutdown) to upload the per-call work lists.  Calls are thread-safe.
+ * device memory; it keeps a small pinned, device-mapped host staging ring (created
+ * lazily, released by tide_shutdown) from which a copy kernel on `stream` moves each
+ * call's work list into the workspace.  Calls are thread-safe.
  */
 #ifndef TIDE_H_
 #define TIDE_H_

@@ -1,6 +1,6 @@
 // The extern "C" entry points declared in include/tide.h: validation and planning on the
-// host (plan.cpp), one host-to-device copy of the work lists into the caller's
-// workspace from a pinned staging ring, then the kernel launches on the caller's stream.
+// host (plan.cpp), a copy kernel that moves the work lists from a pinned staging ring
+// into the caller's workspace, then the kernel launches, all on the caller's stream.
 #include <hip/hip_runtime.h>
 #include <stdlib.h>
 #include <string.h>
@@ -17,18 +17,30 @@
 namespace tide {
 namespace {
 
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
 constexpr int kStagingSlots = 16;
 constexpr size_t kStagingMin = 64 * 1024;
 
-// Pinned host buffers the work lists are copied from.  A slot is reused only after the
-// event recorded behind its previous copy has completed, so a call never overwrites
-// bytes a queued copy has yet to read.
+// Pinned, device-mapped host buffers the work lists are staged in.  A kernel on the
+// caller's stream copies a slot into the workspace (no DMA-engine copy, so no hand-off
+// between engines on every call).  A slot is reused only after the event recorded
+// behind that copy has completed, so a call never overwrites bytes a queued copy has
+// yet to read.
 struct StagingSlot {
   void* host = nullptr;
+  const void* dev = nullptr;  // the same memory as seen from the device
   size_t cap = 0;
   hipEvent_t done = nullptr;
   bool pending = false;
 };
+
+// 16 bytes per thread from the staging slot (host memory) into the workspace.
+__global__ __launch_bounds__(256) void stage_copy_kernel(u32x4_t* dst, const u32x4_t* src,
+                                                         size_t n16) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n16) dst[i] = src[i];
+}
 
 struct DeviceStaging {
   StagingSlot slots[kStagingSlots];
@@ -58,18 +70,28 @@ int upload(const Plan& plan, void* workspace, hipStream_t stream) {
     if (hipEventSynchronize(s.done) != hipSuccess) return TIDE_ERR_HIP;
     s.pending = false;
   }
-  const size_t need = plan.blob.size();
+  const size_t need = plan.blob.size();  // a multiple of kWsAlign
   if (s.cap < need) {
     if (s.host) (void)hipHostFree(s.host);
     s.host = nullptr;
+    s.dev = nullptr;
     s.cap = 0;
-    const size_t cap = std::max(kStagingMin, need + need / 4);
-    if (hipHostMalloc(&s.host, cap, hipHostMallocDefault) != hipSuccess) return TIDE_ERR_HIP;
+    const size_t cap = std::max(kStagingMin, align_up(need + need / 4, kWsAlign));
+    if (hipHostMalloc(&s.host, cap, hipHostMallocMapped) != hipSuccess) return TIDE_ERR_HIP;
+    void* dev_ptr = nullptr;
+    if (hipHostGetDevicePointer(&dev_ptr, s.host, 0) != hipSuccess) {
+      (void)hipHostFree(s.host);
+      s.host = nullptr;
+      return TIDE_ERR_HIP;
+    }
+    s.dev = dev_ptr;
     s.cap = cap;
   }
   memcpy(s.host, plan.blob.data(), need);
-  if (hipMemcpyAsync(workspace, s.host, need, hipMemcpyHostToDevice, stream) != hipSuccess)
-    return TIDE_ERR_HIP;
+  const size_t n16 = need / 16;
+  hipLaunchKernelGGL(stage_copy_kernel, dim3((unsigned)((n16 + 255) / 256)), dim3(256), 0, stream,
+                     static_cast<u32x4_t*>(workspace), static_cast<const u32x4_t*>(s.dev), n16);
+  if (hipGetLastError() != hipSuccess) return TIDE_ERR_HIP;
   if (hipEventRecord(s.done, stream) != hipSuccess) return TIDE_ERR_HIP;
   s.pending = true;
   return TIDE_OK;
