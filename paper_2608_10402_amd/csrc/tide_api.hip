@@ -20,7 +20,9 @@ namespace {
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kStagingSlots = 16;
-constexpr size_t kStagingMin = 64 * 1024;
+// Slots start large and grow by powers of two, so that steady-state calls never
+// reallocate: freeing and allocating pinned memory is slow and can stall the device.
+constexpr size_t kStagingMin = 2u << 20;
 
 // Pinned, device-mapped host buffers the work lists are staged in.  A kernel on the
 // caller's stream copies a slot into the workspace (no DMA-engine copy, so no hand-off
@@ -76,7 +78,8 @@ int upload(const Plan& plan, void* workspace, hipStream_t stream) {
     s.host = nullptr;
     s.dev = nullptr;
     s.cap = 0;
-    const size_t cap = std::max(kStagingMin, align_up(need + need / 4, kWsAlign));
+    size_t cap = kStagingMin;
+    while (cap < need) cap *= 2;
     if (hipHostMalloc(&s.host, cap, hipHostMallocMapped) != hipSuccess) return TIDE_ERR_HIP;
     void* dev_ptr = nullptr;
     if (hipHostGetDevicePointer(&dev_ptr, s.host, 0) != hipSuccess) {
