@@ -15,6 +15,9 @@ U{2048..16384}, observations log-uniform 64..2048, fragmented page placement):
     1. KV-append of each task's decoded token, 2. split-K decode over its context
   long_horizon
     1. KV-append of the new tokens, 2. extend, 3. eight rounds of (append one token, decode)
+  grpo_group_decode
+    1. KV-append of each trajectory's decoded token, 2. shared-prefix decode
+       (tide_decode_attn_shared), 3. plain decode of the same tokens, for comparison
 
 Inputs are resident in HBM before timing starts.  `ms_per_step` comes from HIP events
 around K whole steps on the stream the library launches on.  Each stage is then repeated
@@ -23,7 +26,8 @@ upload, its kernels and launch gaps included); the rates below use those times.
 
 Printed: one JSON line.  For extend workloads `value` is extend-attention throughput in
 TFLOP/s over the unmasked (query, key) pairs (4*d flops per pair and query head); for
-resumed_decode it is decode-attention GB/s of algorithmic bytes.  The line also carries
+resumed_decode it is decode-attention GB/s of algorithmic bytes, and for grpo_group_decode
+the shared-prefix decode's GB/s over the bytes it must read (each prompt once per group).  The line also carries
 the other stages' rates, the speedup of extend over re-prefill, the roofline of the
 dominant kernel, and the fp64 oracle timed on a bounded sample on the host.
 """
@@ -84,6 +88,20 @@ def decode_bytes(wl, kv_lens) -> float:
     kv = float(np.sum(kv_lens)) * s.num_kv_heads * s.head_dim * 2 * 2  # K and V once
     qo = wl.num_tasks * s.num_q_heads * s.head_dim * 2 * 2              # Q in, O out
     bt = float(np.sum(-(-np.asarray(kv_lens) // 16))) * 4                 # page ids read
+    return kv + qo + bt
+
+
+def shared_decode_bytes(wl) -> float:
+    """Bytes a group-aware decode must read: each group's prompt K/V once, every
+    trajectory's own K/V, Q, O and page ids."""
+    s = wl.spec
+    per_tok = s.num_kv_heads * s.head_dim * 2 * 2
+    sizes = np.diff(wl.group_start)
+    shared = np.repeat(wl.shared_lens, sizes).astype(np.float64)
+    own = wl.seq_lens.astype(np.float64) - shared
+    kv = (float(np.sum(wl.shared_lens)) + float(np.sum(own))) * per_tok
+    qo = wl.num_tasks * s.num_q_heads * s.head_dim * 2 * 2
+    bt = float(np.sum(-(-wl.seq_lens // 16))) * 4
     return kv + qo + bt
 
 
@@ -190,6 +208,19 @@ def build_stages(wl, kv, dev, args, torch, np_up):
                                 bytes_=append_bytes(wl, int(wl.seq_lens.sum()))))
             stages.append(Stage("prefill", lambda: kv.prefill(q_full, wl.seq_lens, out=out_full),
                                 flops=prefill_flops(wl)))
+    elif s.kind == "group_decode":
+        k_new, v_new = np_up(wl.packed("k", wl.extend_ranges())), np_up(wl.packed("v", wl.extend_ranges()))
+        q_dec = np_up(wl.packed("q", wl.extend_ranges()))
+        out_s, out_p = torch.empty_like(q_dec), torch.empty_like(q_dec)
+        stages.append(Stage("append_new", lambda: kv.append(k_new, v_new, wl.prefix_lens, wl.extend_lens),
+                            bytes_=append_bytes(wl, wl.num_tasks)))
+        stages.append(Stage("shared_decode",
+                            lambda: kv.decode_shared(q_dec, wl.seq_lens, wl.group_start,
+                                                     wl.shared_lens, out=out_s),
+                            bytes_=shared_decode_bytes(wl)))
+        stages.append(Stage("plain_decode", lambda: kv.decode(q_dec, wl.seq_lens, out=out_p),
+                            bytes_=decode_bytes(wl, wl.seq_lens)))
+        keep.update(out_shared=out_s, out_plain=out_p)
     elif s.kind == "decode":
         k_new, v_new = np_up(wl.packed("k", wl.extend_ranges())), np_up(wl.packed("v", wl.extend_ranges()))
         q_dec = np_up(wl.packed("q", wl.extend_ranges()))
@@ -236,7 +267,17 @@ def main():
     kv = tide.PagedKV(wl.num_pages, s.num_q_heads, s.num_kv_heads, s.head_dim, wl.block_table,
                       wl.sm_scale, device=dev)
     zeros = np.zeros(wl.num_tasks, np.int32)
-    if wl.prefix_lens.sum() > 0:
+    if wl.shared_lens is not None:
+        # a group's prompt pages are written once, then each trajectory's own positions
+        shared = np.repeat(wl.shared_lens, np.diff(wl.group_start)).astype(np.int32)
+        first = np.zeros(wl.num_tasks, np.int32)
+        first[wl.group_start[:-1]] = wl.shared_lens
+        rng = [(0, int(n)) for n in first]
+        kv.append(up(wl.packed("k", rng)), up(wl.packed("v", rng)), zeros, first)
+        own = (wl.prefix_lens - shared).astype(np.int32)
+        rng = [(int(a), int(a + n)) for a, n in zip(shared, own)]
+        kv.append(up(wl.packed("k", rng)), up(wl.packed("v", rng)), shared, own)
+    elif wl.prefix_lens.sum() > 0:
         kv.append(up(wl.packed("k", wl.prefix_ranges())), up(wl.packed("v", wl.prefix_ranges())),
                   zeros, wl.prefix_lens)
     stages, keep = build_stages(wl, kv, dev, args, torch, up)
@@ -309,15 +350,35 @@ def main():
                                "unit": "GB/s", "frac": round(v / PEAK_HBM_GBS, 4)}
         n_dec = sum(1 for k in ms if k.startswith("decode"))
         extra["decode_tokens_per_s"] = round(n_dec * wl.num_tasks / (t * 1e-3), 1)
+    if "shared_decode" in ms:
+        t_s, t_p = ms["shared_decode"], ms["plain_decode"]
+        st_s = [st for st in stages if st.name == "shared_decode"][0]
+        st_p = [st for st in stages if st.name == "plain_decode"][0]
+        v = st_s.bytes / (t_s * 1e-3) / 1e9
+        rooflines["shared_decode"] = {"bound": "hbm", "achieved": round(v, 1), "peak": PEAK_HBM_GBS,
+                                      "unit": "GB/s", "frac": round(v / PEAK_HBM_GBS, 4)}
+        vp = st_p.bytes / (t_p * 1e-3) / 1e9
+        rooflines["plain_decode"] = {"bound": "hbm", "achieved": round(vp, 1), "peak": PEAK_HBM_GBS,
+                                     "unit": "GB/s", "frac": round(vp / PEAK_HBM_GBS, 4)}
+        extra.update({
+            "speedup_shared_vs_plain_decode": round(t_p / t_s, 3),
+            "shared_decode_plain_equivalent_GBps": round(st_p.bytes / (t_s * 1e-3) / 1e9, 1),
+            "decode_tokens_per_s": round(wl.num_tasks / (t_s * 1e-3), 1),
+            "shared_vs_plain_max_abs_diff": float((keep["out_shared"].float() -
+                                                   keep["out_plain"].float()).abs().max().item()),
+        })
     if any(k.startswith("append") for k in ms):
         t, _, b = total("append")
         v = b / (t * 1e-3) / 1e9
         rooflines["append"] = {"bound": "hbm", "achieved": round(v, 1), "peak": PEAK_HBM_GBS,
                                "unit": "GB/s", "frac": round(v / PEAK_HBM_GBS, 4)}
 
-    primary = "extend" if "extend" in rooflines else "decode"
+    primary = ("extend" if "extend" in rooflines else
+               "shared_decode" if "shared_decode" in rooflines else "decode")
     roofline = dict(rooflines[primary])
-    roofline["kernel"] = "extend_attn_kernel" if primary == "extend" else "decode_split_kernel"
+    roofline["kernel"] = {"extend": "extend_attn_kernel<128, false>",
+                          "decode": "decode_split_kernel<128, false>",
+                          "shared_decode": "decode_split_kernel<128, true>"}[primary]
     roofline["traffic"] = counter_traffic(s.key, primary)
 
     cpu = None

@@ -16,6 +16,8 @@
  *     tide_extend_attn        attention of the new tokens over retained prefix + themselves
  *     tide_decode_attn        one query token per task over its whole context (split-K)
  *     tide_full_prefill_attn  causal attention over the whole sequence (the recompute path)
+ *   and one variant of decode for GRPO groups whose trajectories share a prompt prefix:
+ *     tide_decode_attn_shared tide_decode_attn, reading each shared prefix once per group
  *
  *   The attention itself is standard scaled dot-product attention (Vaswani et al.,
  *   2017), which the paper uses but does not restate: for a query row at absolute
@@ -167,6 +169,37 @@ TIDE_API int tide_decode_attn(const void* q, const void* k_pool, const void* v_p
                      const int32_t* kv_lens, const tide_dims* dims, int32_t num_splits,
                      void* out, float* lse, void* workspace, size_t workspace_bytes,
                      void* stream);
+
+/*
+ * Decode attention for tasks grouped by a shared prompt prefix.  GRPO samples a group of
+ * trajectories per task (Section 2.1), and Continuous Task Batching resumes them with
+ * group affinity so that they keep sharing the prefix pages (Section 4.2).  The result
+ * is that of tide_decode_attn on the same arguments; only the pages of a shared prefix
+ * are read once per group of up to 16 / G trajectories instead of once per trajectory.
+ *   group_start  host int32 [num_groups + 1]: group g is tasks group_start[g] ..
+ *                group_start[g+1] - 1 (consecutive, non-empty; group_start[0] == 0,
+ *                group_start[num_groups] == num_tasks; a lone task is a group of one)
+ *   shared_lens  host int32 [num_groups]: the first shared_lens[g] positions of every
+ *                member are the same physical pages (equal leading block-table entries)
+ *                holding the same K/V; a multiple of the page size, at most kv_len - 1 of
+ *                every member (the decoded token is each trajectory's own); 0 = nothing
+ *                shared.  The shared pages are read through the group's first task.
+ * num_splits as in tide_decode_attn (the shared prefix and a task's own keys are split
+ * separately, so a task may get one split more).  Workspace: tide_workspace_size_shared.
+ * Errors: TIDE_ERR_INVALID_ARG for a malformed group table or shared length.
+ */
+TIDE_API int tide_decode_attn_shared(const void* q, const void* k_pool, const void* v_pool,
+                            int64_t num_pages, const int32_t* block_table, int32_t bt_stride,
+                            int32_t num_tasks, const int32_t* kv_lens, int32_t num_groups,
+                            const int32_t* group_start, const int32_t* shared_lens,
+                            const tide_dims* dims, int32_t num_splits, void* out, float* lse,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace tide_decode_attn_shared needs for these host arguments. */
+TIDE_API int tide_workspace_size_shared(int32_t num_tasks, const int32_t* kv_lens,
+                               int32_t num_groups, const int32_t* group_start,
+                               const int32_t* shared_lens, const tide_dims* dims,
+                               int32_t num_splits, size_t* bytes_out);
 
 /*
  * Full re-prefill attention: causal attention over all seq_lens[b] positions of each

@@ -1,6 +1,7 @@
 """Paged-KV resume attention for AMD MI355X (gfx950): the hot path of TideRL's
 Continuous Task Batching (arXiv 2608.10402) -- KV-append, extend attention over a
-retained paged prefix, split-K decode attention, and full re-prefill for comparison.
+retained paged prefix, split-K decode attention (also over prompt prefixes shared by a
+GRPO group), and full re-prefill for comparison.
 
 The compute lives in libtide.so (hand-written HIP kernels behind the C ABI of
 include/tide.h).  This package is its ctypes binding plus a small pool helper.
@@ -8,8 +9,9 @@ include/tide.h).  This package is its ctypes binding plus a small pool helper.
 from ._lib import (TIDE_ERR_CAPACITY, TIDE_ERR_HIP, TIDE_ERR_INVALID_ARG, TIDE_ERR_PAGE_RANGE,
                    TIDE_ERR_UNSUPPORTED, TIDE_OK, TIDE_OP_DECODE, TIDE_OP_EXTEND,
                    TIDE_OP_FULL_PREFILL, TIDE_OP_KV_APPEND, TideError, alloc_workspace, load,
-                   make_dims, status_string, tide_decode_attn, tide_dims, tide_extend_attn,
-                   tide_full_prefill_attn, tide_kv_append, tide_shutdown, tide_workspace_size)
+                   make_dims, status_string, tide_decode_attn, tide_decode_attn_shared, tide_dims,
+                   tide_extend_attn, tide_full_prefill_attn, tide_kv_append, tide_shutdown,
+                   tide_workspace_size, tide_workspace_size_shared)
 from .kvcache import PagedKV
 
 __all__ = ["TIDE_ERR_CAPACITY", "TIDE_ERR_HIP", "TIDE_ERR_INVALID_ARG", "TIDE_ERR_PAGE_RANGE",
@@ -17,4 +19,4 @@ __all__ = ["TIDE_ERR_CAPACITY", "TIDE_ERR_HIP", "TIDE_ERR_INVALID_ARG", "TIDE_ER
            "TIDE_OP_FULL_PREFILL", "TIDE_OP_KV_APPEND", "TideError", "alloc_workspace", "load",
            "make_dims", "status_string", "tide_decode_attn", "tide_dims", "tide_extend_attn",
            "tide_full_prefill_attn", "tide_kv_append", "tide_shutdown", "tide_workspace_size",
-           "PagedKV"]
+           "tide_decode_attn_shared", "tide_workspace_size_shared", "PagedKV"]

@@ -28,7 +28,8 @@ TIDE_OP_DECODE = 3
 TIDE_OP_FULL_PREFILL = 4
 
 EXPORTED = ("tide_workspace_size", "tide_kv_append", "tide_extend_attn", "tide_decode_attn",
-            "tide_full_prefill_attn", "tide_status_string", "tide_shutdown")
+            "tide_full_prefill_attn", "tide_decode_attn_shared", "tide_workspace_size_shared",
+            "tide_status_string", "tide_shutdown")
 
 
 class TideError(RuntimeError):
@@ -71,6 +72,10 @@ def load(path: str = LIB_PATH):
                                      sz, vp]
     lib.tide_full_prefill_attn.argtypes = [vp, vp, vp, i64, vp, i32, i32, vp, dims_p, vp, vp, vp,
                                            sz, vp]
+    lib.tide_decode_attn_shared.argtypes = [vp, vp, vp, i64, vp, i32, i32, vp, i32, vp, vp, dims_p,
+                                            i32, vp, vp, vp, sz, vp]
+    lib.tide_workspace_size_shared.argtypes = [i32, vp, i32, vp, vp, dims_p, i32,
+                                               ctypes.POINTER(sz)]
     for name in EXPORTED[:-2]:
         getattr(lib, name).restype = ctypes.c_int
     lib.tide_status_string.argtypes = [ctypes.c_int]
@@ -198,6 +203,41 @@ def tide_decode_attn(q, k_pool, v_pool, block_table, kv_lens, dims: tide_dims, o
         kv_p, ctypes.byref(dims), int(num_splits), _dev(out, torch.bfloat16, "out"),
         _dev(lse, torch.float32, "lse", nullable=True), ws, ws_n, _stream(stream)),
         "tide_decode_attn")
+
+
+def _groups(group_start, shared_lens):
+    gs, gs_p = _host(group_start, "group_start")
+    sh, sh_p = _host(shared_lens, "shared_lens")
+    if gs is None or sh is None or gs.size != sh.size + 1:
+        raise ValueError("group_start must have one entry more than shared_lens")
+    return int(sh.size), gs, gs_p, sh, sh_p
+
+
+def tide_workspace_size_shared(kv_lens, group_start, shared_lens, dims: tide_dims,
+                               num_splits: int = 0) -> int:
+    kv, kv_p = _host(kv_lens, "kv_lens")
+    ng, gs, gs_p, sh, sh_p = _groups(group_start, shared_lens)
+    out = ctypes.c_size_t(0)
+    _check(load().tide_workspace_size_shared(int(kv.size), kv_p, ng, gs_p, sh_p,
+                                             ctypes.byref(dims), int(num_splits),
+                                             ctypes.byref(out)), "tide_workspace_size_shared")
+    return int(out.value)
+
+
+def tide_decode_attn_shared(q, k_pool, v_pool, block_table, kv_lens, group_start, shared_lens,
+                            dims: tide_dims, out, lse=None, num_splits: int = 0, workspace=None,
+                            stream=None) -> None:
+    num_pages = _pool_shape(k_pool, v_pool, dims)
+    kv, kv_p = _host(kv_lens, "kv_lens")
+    ng, gs, gs_p, sh, sh_p = _groups(group_start, shared_lens)
+    ws, ws_n = _ws(workspace)
+    _check(load().tide_decode_attn_shared(
+        _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"),
+        _dev(v_pool, torch.bfloat16, "v_pool"), num_pages,
+        _dev(block_table, torch.int32, "block_table"), int(block_table.shape[1]), int(kv.size),
+        kv_p, ng, gs_p, sh_p, ctypes.byref(dims), int(num_splits),
+        _dev(out, torch.bfloat16, "out"), _dev(lse, torch.float32, "lse", nullable=True), ws,
+        ws_n, _stream(stream)), "tide_decode_attn_shared")
 
 
 def tide_full_prefill_attn(q, k_pool, v_pool, block_table, seq_lens, dims: tide_dims, out,

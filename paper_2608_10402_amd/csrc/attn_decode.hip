@@ -8,6 +8,12 @@
 //   * One wave per (task, kv head, chunk).  The G query heads of the kv head share every
 //     K/V load; they are the columns of v_mfma_f32_16x16x32_bf16 (G <= 16), so the
 //     contraction costs a few MFMA issues per 2 KB loaded and no VALU dot products.
+//   * Shared-prefix variant (a GRPO group's trajectories share their task's prompt pages,
+//     TideRL Section 2.1; CTB keeps them on one rank, Section 4.2): a chunk of the shared
+//     prefix is one wave for several trajectories, whose (trajectory, head) pairs fill the
+//     16 MFMA columns, so the prefix is read once per group of trajectories instead of
+//     once per trajectory.  Each trajectory's own keys are ordinary chunks; all of them are
+//     splits of the same merge.
 //   * Operands go straight from HBM into MFMA registers (no LDS): for S^T = K.Q^T a lane
 //     loads 16 contiguous bytes of one key row; for O^T += V^T.P^T it loads two 8-byte
 //     pieces of transposed V pages (4 consecutive token slots of one head-dim entry in
@@ -67,7 +73,10 @@ __device__ __forceinline__ uint2 keep_first4(uint2 x, int n) {
   return r;
 }
 
-template <int D>
+// kShared: the items are SharedDecodeItem: keys of a prefix shared by ntasks tasks (the
+// MFMA columns are then (task, query head) pairs, ntasks * G <= 16, so every K/V byte is
+// loaded once for all of them), or a task's own keys after it.  Otherwise DecodeItem.
+template <int D, bool kShared>
 __global__ __launch_bounds__(kWavesPerBlock * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void decode_split_kernel(DecodeArgs a) {
   const int lane = threadIdx.x & 63;
@@ -75,26 +84,47 @@ void decode_split_kernel(DecodeArgs a) {
   // derived from it stay scalar
   const int item_id = blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (item_id >= a.num_items) return;  // whole wave exits; no block-level barrier below
-  const DecodeItem it = a.items[item_id];
-  const TaskDesc td = a.tasks[it.task];
+  int first_task, ntasks, kv_head, split, kbeg, kend;
+  if constexpr (kShared) {
+    const SharedDecodeItem it = static_cast<const SharedDecodeItem*>(a.items)[item_id];
+    first_task = it.first_task;
+    ntasks = it.ntasks;
+    kv_head = it.kv_head;
+    split = it.split;
+    kbeg = it.k_begin;
+    kend = it.k_end;
+  } else {
+    const DecodeItem it = static_cast<const DecodeItem*>(a.items)[item_id];
+    first_task = it.task;
+    ntasks = 1;
+    kv_head = it.kv_head;
+    split = it.split;
+    kbeg = it.k_begin;
+  }
+  const TaskDesc td = a.tasks[first_task];
   const int kv_len = td.prefix + td.extend;
+  if constexpr (!kShared) kend = min(kv_len, kbeg + a.chunk);
   const int npages = (kv_len + kPage - 1) / kPage;
-  const int32_t* bt_row = a.block_table + (int64_t)it.task * a.bt_stride;
+  const int32_t* bt_row = a.block_table + (int64_t)first_task * a.bt_stride;
   const int G = a.group;
   const int col = lane & 15, grp = lane >> 4;
+  const int kv_h = kv_head;
   const uint8_t* kpool = reinterpret_cast<const uint8_t*>(a.k_pool);
   const uint8_t* vpool = reinterpret_cast<const uint8_t*>(a.v_pool);
   constexpr int64_t kBlk = (int64_t)kPage * D * 2;  // bytes of one (page, kv head) block
 
-  // Q^T operand: column col = query head kv_head*G + col (zero when col >= G)
+  // Column col: task first_task + col / G, query head kv_head * G + col % G (no column
+  // past ntasks * G: its Q is zero and nothing is written for it)
+  const bool col_ok = col < ntasks * G;
+  const int ctask = kShared ? first_task + col / G : first_task;
+  const int chead = kShared ? col % G : col;
+  const int crow = kShared ? (col_ok ? a.tasks[ctask].row_start : 0) : td.row_start;
   bf16x8 qf[D / 32];
-  const int64_t qrow = (int64_t)td.row_start * a.num_q_heads + it.kv_head * G + col;
+  const int64_t qrow = (int64_t)crow * a.num_q_heads + kv_h * G + chead;
 #pragma unroll
   for (int c = 0; c < D / 32; ++c)
-    qf[c] = as_bf16x8(col < G ? load_u32x4(a.q + qrow * D + 32 * c + 8 * grp) : zero_u32x4());
+    qf[c] = as_bf16x8(col_ok ? load_u32x4(a.q + qrow * D + 32 * c + 8 * grp) : zero_u32x4());
 
-  const int kbeg = it.k_begin;
-  const int kend = min(kv_len, kbeg + a.chunk);
   const uint32_t k_off = (uint32_t)(col * D * 2 + 16 * grp);       // token slot `col`
   const uint32_t v_off = (uint32_t)(col * kPage * 2 + 8 * grp);    // head-dim row `col`
 
@@ -111,7 +141,7 @@ void decode_split_kernel(DecodeArgs a) {
     const int32_t p = __builtin_amdgcn_readlane(pid, lp - lp_batch);
     const bool bad = p < 0 || p >= a.num_pages || lp >= npages;
     // pages past the context (and invalid ids) read page 0: masked / zeroed below
-    const int64_t blk = ((int64_t)(bad ? 0 : p) * a.num_kv_heads + it.kv_head) * kBlk;
+    const int64_t blk = ((int64_t)(bad ? 0 : p) * a.num_kv_heads + kv_h) * kBlk;
     if (bad && lp < npages) flag_error = true;
     return blk;
   };
@@ -136,23 +166,24 @@ void decode_split_kernel(DecodeArgs a) {
 #pragma unroll
       for (int c = 0; c < D / 32; ++c) s[t] = mfma16(as_bf16x8(cur.k[t][c]), qf[c], s[t]);
     }
-    const bool tail = k + 2 * kPage > kv_len;
+    // keys at or past kend (the context's end, or the shared prefix's) are not this item's
+    const bool tail = k + 2 * kPage > kend;
     float mt = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         float x = s[t][e] * a.scale_log2;
-        if (tail) x = (k + 16 * t + 4 * grp + e < kv_len) ? x : -INFINITY;
+        if (tail) x = (k + 16 * t + 4 * grp + e < kend) ? x : -INFINITY;
         s[t][e] = x;
         mt = fmaxf(mt, x);
       }
-    if (tail) {  // V slots past the context must not reach the MFMA (NaN * 0 = NaN)
+    if (tail) {  // V slots past kend must not reach the MFMA (NaN * 0 = NaN)
 #pragma unroll
       for (int t = 0; t < D / 16; ++t)
 #pragma unroll
         for (int hp = 0; hp < 2; ++hp)
-          cur.v[t][hp] = keep_first4(cur.v[t][hp], kv_len - (k + 16 * hp + 4 * grp));
+          cur.v[t][hp] = keep_first4(cur.v[t][hp], kend - (k + 16 * hp + 4 * grp));
     }
     mt = fmaxf(mt, xor_shfl(mt, 16));
     mt = fmaxf(mt, xor_shfl(mt, 32));
@@ -201,9 +232,9 @@ void decode_split_kernel(DecodeArgs a) {
   l_tot += xor_shfl(l_tot, 32);
   float l_ex = l_exact + xor_shfl(l_exact, 16);
   l_ex += xor_shfl(l_ex, 32);
-  if (col < G) {
+  if (col_ok) {
     const int64_t slot =
-        ((int64_t)it.task * a.num_q_heads + it.kv_head * G + col) * a.max_splits + it.split;
+        ((int64_t)ctask * a.num_q_heads + kv_h * G + chead) * a.max_splits + split;
     float* po = a.part_o + slot * D;
 #pragma unroll
     for (int t = 0; t < D / 16; ++t)
@@ -282,12 +313,12 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_merge_kernel(Decod
   }
 }
 
-template <int D>
+template <int D, bool kShared>
 hipError_t launch(const DecodeArgs& a, hipStream_t stream) {
   if (a.num_items > 0) {
     const int blocks = (a.num_items + kWavesPerBlock - 1) / kWavesPerBlock;
-    hipLaunchKernelGGL((decode_split_kernel<D>), dim3(blocks), dim3(kWavesPerBlock * 64), 0,
-                       stream, a);
+    hipLaunchKernelGGL((decode_split_kernel<D, kShared>), dim3(blocks), dim3(kWavesPerBlock * 64),
+                       0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -300,11 +331,20 @@ hipError_t launch(const DecodeArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// Both variants of each head size are instantiated explicitly: the host pass otherwise
+// emits the launch stub of only one of two specialisations that differ in the bool.
+template __global__ void decode_split_kernel<128, false>(DecodeArgs);
+template __global__ void decode_split_kernel<128, true>(DecodeArgs);
+template __global__ void decode_split_kernel<64, false>(DecodeArgs);
+template __global__ void decode_split_kernel<64, true>(DecodeArgs);
+
 }  // namespace kern
 
-hipError_t launch_decode(const DecodeArgs& a, int head_dim, hipStream_t stream) {
-  if (head_dim == 128) return kern::launch<128>(a, stream);
-  if (head_dim == 64) return kern::launch<64>(a, stream);
+hipError_t launch_decode(const DecodeArgs& a, int head_dim, bool shared, hipStream_t stream) {
+  if (head_dim == 128)
+    return shared ? kern::launch<128, true>(a, stream) : kern::launch<128, false>(a, stream);
+  if (head_dim == 64)
+    return shared ? kern::launch<64, true>(a, stream) : kern::launch<64, false>(a, stream);
   return hipErrorInvalidValue;
 }
 

@@ -9,6 +9,6 @@ namespace tide {
 
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_extend(const ExtendArgs& a, int head_dim, int waves, hipStream_t stream);
-hipError_t launch_decode(const DecodeArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs& a, int head_dim, bool shared, hipStream_t stream);
 
 }  // namespace tide

@@ -249,4 +249,118 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
   return TIDE_OK;
 }
 
+int make_plan_shared(int32_t num_tasks, const int32_t* kv_lens, int32_t num_groups,
+                     const int32_t* group_start, const int32_t* shared_lens,
+                     const tide_dims& dims, int32_t num_splits, int32_t bt_stride,
+                     bool build_blob, Plan* plan) {
+  if (!plan) return TIDE_ERR_INVALID_ARG;
+  int rc = check_dims(&dims);
+  if (rc != TIDE_OK) return rc;
+  if (num_tasks < 0 || num_splits < 0 || num_groups < 0) return TIDE_ERR_INVALID_ARG;
+  *plan = Plan();
+  plan->op = kOpDecodeShared;
+  plan->num_tasks = num_tasks;
+  if (num_tasks > 0) {
+    if (!kv_lens || !group_start || !shared_lens || num_groups < 1) return TIDE_ERR_INVALID_ARG;
+    if (group_start[0] != 0 || group_start[num_groups] != num_tasks) return TIDE_ERR_INVALID_ARG;
+  }
+  const int32_t group = dims.num_q_heads / dims.num_kv_heads;
+  const int32_t per_item = std::max<int32_t>(1, 16 / group);  // trajectories per prefix item
+
+  std::vector<TaskDesc> tasks((size_t)num_tasks);
+  std::vector<int32_t> shared_of((size_t)num_tasks, 0);
+  for (int32_t g = 0; g < (num_tasks > 0 ? num_groups : 0); ++g) {
+    const int32_t s0 = group_start[g], s1 = group_start[g + 1];
+    const int32_t sh = shared_lens[g];
+    if (s1 <= s0 || s1 > num_tasks) return TIDE_ERR_INVALID_ARG;
+    if (sh < 0 || sh % kPage != 0) return TIDE_ERR_INVALID_ARG;
+    for (int32_t b = s0; b < s1; ++b) {
+      if (kv_lens[b] <= 0 || sh > kv_lens[b] - 1) return TIDE_ERR_INVALID_ARG;
+      if (bt_stride >= 0 && ceil_div(kv_lens[b], kPage) > bt_stride) return TIDE_ERR_CAPACITY;
+      tasks[b] = TaskDesc{b, kv_lens[b] - 1, 1, 0};
+      shared_of[b] = sh;
+    }
+  }
+  plan->total_rows = num_tasks;
+
+  // Chunk length: the same rule as decode, counting a shared prefix once per item group.
+  int64_t chunk = 0;
+  if (num_splits > 0) {
+    for (int32_t b = 0; b < num_tasks; ++b)
+      chunk = std::max<int64_t>(chunk, ceil_div(kv_lens[b], num_splits));
+    chunk = std::max<int64_t>(kDecodeStep, ceil_div(chunk, kDecodeStep) * kDecodeStep);
+  } else {
+    int64_t total = 0;
+    for (int32_t g = 0; g < (num_tasks > 0 ? num_groups : 0); ++g) {
+      const int32_t n = group_start[g + 1] - group_start[g];
+      total += ceil_div(n, per_item) * (int64_t)shared_lens[g];
+    }
+    for (int32_t b = 0; b < num_tasks; ++b) total += (int64_t)kv_lens[b] - shared_of[b];
+    total *= dims.num_kv_heads;
+    chunk = ceil_div(total, 8192);
+    chunk = ceil_div(chunk, kDecodeStep) * kDecodeStep;
+    chunk = std::min<int64_t>(std::max<int64_t>(chunk, 256), 16384);
+  }
+
+  std::vector<SharedDecodeItem> items;
+  int32_t max_splits = 0;
+  for (int32_t g = 0; g < (num_tasks > 0 ? num_groups : 0); ++g) {
+    const int32_t s0 = group_start[g], s1 = group_start[g + 1], sh = shared_lens[g];
+    const int32_t np = (int32_t)ceil_div(sh, chunk);
+    for (int32_t f = s0; f < s1; f += per_item)
+      for (int32_t h = 0; h < dims.num_kv_heads; ++h)
+        for (int32_t j = 0; j < np; ++j) {
+          SharedDecodeItem it = {};
+          it.first_task = f;
+          it.ntasks = std::min(per_item, s1 - f);
+          it.kv_head = h;
+          it.split = j;
+          it.k_begin = (int32_t)(j * chunk);
+          it.k_end = (int32_t)std::min<int64_t>(sh, (j + 1) * chunk);
+          items.push_back(it);
+        }
+    for (int32_t b = s0; b < s1; ++b) {
+      const int32_t ns = (int32_t)ceil_div((int64_t)kv_lens[b] - sh, chunk);
+      tasks[b].aux = np + ns;
+      max_splits = std::max(max_splits, np + ns);
+      for (int32_t h = 0; h < dims.num_kv_heads; ++h)
+        for (int32_t i = 0; i < ns; ++i) {
+          SharedDecodeItem it = {};
+          it.first_task = b;
+          it.ntasks = 1;
+          it.kv_head = h;
+          it.split = np + i;
+          it.k_begin = (int32_t)(sh + i * chunk);
+          it.k_end = (int32_t)std::min<int64_t>(kv_lens[b], sh + (i + 1) * chunk);
+          items.push_back(it);
+        }
+    }
+  }
+  if ((int64_t)items.size() > INT32_MAX / 4) return TIDE_ERR_INVALID_ARG;
+  plan->chunk = (int32_t)chunk;
+  plan->max_splits = max_splits;
+  plan->num_items = (int32_t)items.size();
+
+  size_t off = sizeof(WsHeader);
+  plan->tasks_off = off;
+  off = align_up(off + tasks.size() * sizeof(TaskDesc), kWsAlign);
+  plan->items_off = off;
+  off = align_up(off + items.size() * sizeof(SharedDecodeItem), kWsAlign);
+  plan->upload_bytes = off;
+  const size_t slots = (size_t)num_tasks * dims.num_q_heads * (size_t)max_splits;
+  plan->part_o_off = off;
+  off = align_up(off + slots * dims.head_dim * sizeof(float), kWsAlign);
+  plan->part_ml_off = off;
+  off = align_up(off + slots * 4 * sizeof(float), kWsAlign);
+  plan->total_bytes = off;
+  if (build_blob) {
+    plan->blob.assign(plan->upload_bytes, 0);
+    if (!tasks.empty())
+      memcpy(plan->blob.data() + plan->tasks_off, tasks.data(), tasks.size() * sizeof(TaskDesc));
+    if (!items.empty())
+      memcpy(plan->blob.data() + plan->items_off, items.data(), items.size() * sizeof(SharedDecodeItem));
+  }
+  return TIDE_OK;
+}
+
 }  // namespace tide

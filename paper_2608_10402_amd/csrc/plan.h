@@ -45,6 +45,15 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
               const tide_dims& dims, int32_t num_splits, int32_t bt_stride, bool build_blob,
               Plan* plan);
 
+// Shared-prefix decode: groups are consecutive task ranges [group_start[g],
+// group_start[g+1]); the first shared_lens[g] keys (a multiple of the page size, below
+// every member's kv_len) live in pages every member's block table shares.
+constexpr int kOpDecodeShared = 100;  // internal op code of the plan
+int make_plan_shared(int32_t num_tasks, const int32_t* kv_lens, int32_t num_groups,
+                     const int32_t* group_start, const int32_t* shared_lens,
+                     const tide_dims& dims, int32_t num_splits, int32_t bt_stride,
+                     bool build_blob, Plan* plan);
+
 // Waves per workgroup of the extend kernel for a head size and GQA group.
 int32_t extend_waves(int32_t head_dim, int32_t group);
 

@@ -40,6 +40,20 @@ struct DecodeItem {
   int32_t k_begin;
 };
 
+// Shared-prefix decode item: keys [k_begin, k_end) for tasks first_task ..
+// first_task + ntasks - 1 and one kv head.  With ntasks > 1 the keys lie in the prefix
+// the tasks share (the same physical pages, read through first_task's block table), and
+// the item writes one split partial per task; ntasks * group <= 16.
+struct SharedDecodeItem {
+  int32_t first_task;
+  int32_t ntasks;
+  int32_t kv_head;
+  int32_t split;
+  int32_t k_begin;
+  int32_t k_end;
+  int32_t pad[2];
+};
+
 // Append item: positions [pos_begin, pos_end) of `task`, all inside logical page `lpage`.
 struct AppendItem {
   int32_t task;
@@ -105,7 +119,7 @@ struct DecodeArgs {
   int32_t chunk;       // keys per split (multiple of kDecodeStep)
   int32_t max_splits;  // split slots per (task, q head) in the partial buffers
   const TaskDesc* tasks;  // prefix + extend == kv_len, aux == number of splits
-  const DecodeItem* items;
+  const void* items;      // DecodeItem, or SharedDecodeItem for the shared-prefix variant
   float* part_o;   // [num_tasks][Hq][max_splits][d] unnormalised partial outputs
   float* part_ml;  // [num_tasks][Hq][max_splits][4]: max (base-2 units), sum of the
                    // bf16-rounded weights, exact fp32 sum, unused

@@ -74,6 +74,16 @@ class PagedKV:
                               out, lse, num_splits, ws, stream)
         return out
 
+    def decode_shared(self, q, kv_lens, group_start, shared_lens, num_splits: int = 0, out=None,
+                      lse=None, stream=None):
+        out = torch.empty_like(q) if out is None else out
+        ws = self.workspace(_lib.tide_workspace_size_shared(kv_lens, group_start, shared_lens,
+                                                            self.dims, num_splits))
+        _lib.tide_decode_attn_shared(q, self.k_pool, self.v_pool, self.block_table, kv_lens,
+                                     group_start, shared_lens, self.dims, out, lse, num_splits,
+                                     ws, stream)
+        return out
+
     def prefill(self, q, seq_lens, out=None, lse=None, stream=None):
         out = torch.empty_like(q) if out is None else out
         ws = self.workspace(_lib.tide_workspace_size(_lib.TIDE_OP_FULL_PREFILL, seq_lens, None,

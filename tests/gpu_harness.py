@@ -48,7 +48,22 @@ class DeviceWorkload:
         self.kv = tide.PagedKV(wl.num_pages, s.num_q_heads, s.num_kv_heads, s.head_dim,
                                wl.block_table, wl.sm_scale, device=device)
         zeros = np.zeros(wl.num_tasks, np.int32)
-        if wl.prefix_lens.sum() > 0:
+        if wl.shared_lens is not None:
+            # GRPO groups: a group's prompt pages are written once (through its first
+            # task), then every trajectory's own positions up to the decoded token
+            shared = np.repeat(wl.shared_lens, np.diff(wl.group_start)).astype(np.int32)
+            first = np.zeros(wl.num_tasks, np.int32)
+            first[wl.group_start[:-1]] = wl.shared_lens
+            rng = [(0, int(n)) for n in first]
+            if first.sum() > 0:
+                self.kv.append(dev_bf16(wl.packed("k", rng)), dev_bf16(wl.packed("v", rng)),
+                               zeros, first)
+            own = (wl.prefix_lens - shared).astype(np.int32)
+            rng = [(int(a), int(a + n)) for a, n in zip(shared, own)]
+            if own.sum() > 0:
+                self.kv.append(dev_bf16(wl.packed("k", rng)), dev_bf16(wl.packed("v", rng)),
+                               shared, own)
+        elif wl.prefix_lens.sum() > 0:
             self.kv.append(dev_bf16(wl.packed("k", wl.prefix_ranges())),
                            dev_bf16(wl.packed("v", wl.prefix_ranges())), zeros, wl.prefix_lens)
 

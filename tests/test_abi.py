@@ -161,3 +161,62 @@ def test_binding_rejects_host_tensors():
     q = torch.zeros(4, 8, 64, dtype=torch.bfloat16)
     with pytest.raises((ValueError, TypeError)):
         tide.tide_extend_attn(q, q, q, q, [1], [1], _lib.make_dims(8, 2, 64, 0.1), q)
+
+
+# ---- shared-prefix decode -------------------------------------------------------------------
+def _ws_shared(kv, gs, sh, dims, splits=0):
+    return _lib.tide_workspace_size_shared(kv, gs, sh, dims, splits)
+
+
+def test_shared_decode_validation():
+    dims = tide.make_dims(32, 8, 128, 1.0 / math.sqrt(128))
+    kv = [100, 120, 80, 300]
+    ok = _ws_shared(kv, [0, 2, 3, 4], [64, 48, 0], dims)
+    assert ok > 0
+    bad_tables = [
+        ([1, 2, 3, 4], [64, 48, 0]),   # does not start at 0
+        ([0, 2, 3, 3], [64, 48, 0]),   # empty group / does not end at num_tasks
+        ([0, 3, 2, 4], [64, 48, 0]),   # not increasing
+        ([0, 2, 3, 4], [60, 48, 0]),   # shared length not a page multiple
+        ([0, 2, 3, 4], [112, 48, 0]),  # shared beyond kv_len - 1 of task 0 (100)
+        ([0, 2, 3, 4], [64, 80, 0]),   # shared == kv_len of task 2: the decoded token is its own
+        ([0, 2, 3, 4], [64, -16, 0]),  # negative
+    ]
+    for gs, sh in bad_tables:
+        with pytest.raises(tide.TideError) as e:
+            _ws_shared(kv, gs, sh, dims)
+        assert e.value.status == tide.TIDE_ERR_INVALID_ARG, (gs, sh)
+    with pytest.raises(ValueError):
+        _ws_shared(kv, [0, 4], [0, 0], dims)  # group_start must be one longer than shared_lens
+
+
+def test_shared_decode_workspace_covers_splits():
+    """With nothing shared, the shared-prefix plan has the plain decode's split count, so
+    its workspace is the plain one plus the larger work items."""
+    dims = tide.make_dims(32, 8, 128, 1.0 / math.sqrt(128))
+    rng = np.random.default_rng(5)
+    kv = rng.integers(1, 5000, size=37)
+    rc, plain = _ws(tide.TIDE_OP_DECODE, kv, None, dims)
+    assert rc == tide.TIDE_OK
+    shared0 = _ws_shared(kv, np.arange(38), np.zeros(37, np.int32), dims)
+    assert shared0 >= plain
+    # a shared prefix adds at most one split per task
+    gs = [0, 10, 20, 37]
+    sh = [min(kv[0:10].min() - 1, 1024) // 16 * 16, min(kv[10:20].min() - 1, 512) // 16 * 16, 0]
+    assert _ws_shared(kv, gs, sh, dims) > 0
+
+
+def test_shared_decode_rejects_before_gpu():
+    """Argument errors are reported without any device work (this runs on the CPU)."""
+    lib = tide.load()
+    dims = tide.make_dims(32, 8, 128, 1.0 / math.sqrt(128))
+    kv = np.array([40, 50], np.int32)
+    gs = np.array([0, 2], np.int32)
+    sh = np.array([48], np.int32)  # 48 > 40 - 1
+    rc = lib.tide_decode_attn_shared(None, None, None, 10, None, 4, 2, kv.ctypes.data, 1,
+                                     gs.ctypes.data, sh.ctypes.data, ctypes.byref(dims), 0, None,
+                                     None, None, 0, None)
+    assert rc == tide.TIDE_ERR_INVALID_ARG
+    rc = lib.tide_decode_attn_shared(None, None, None, 10, None, 4, 0, None, 0, None, None,
+                                     ctypes.byref(dims), 0, None, None, None, 0, None)
+    assert rc == tide.TIDE_OK  # no tasks: nothing to do

@@ -44,7 +44,14 @@ def test_workload_shapes(key):
         row = wl.block_table[b]
         assert (row[:n] >= 0).all() and (row[:n] < wl.num_pages).all()
         assert (row[n:] == -1).all()
-        used.extend(row[:n].tolist())
+        sp = 0 if wl.shared_lens is None else int(wl.shared_lens[wl.group_of(b)]) // 16
+        used.extend(row[sp:n].tolist())  # a group's prompt pages are checked below
+    if wl.shared_lens is not None:
+        for g in range(len(wl.shared_lens)):
+            s0, s1 = int(wl.group_start[g]), int(wl.group_start[g + 1])
+            sp = int(wl.shared_lens[g]) // 16
+            assert (wl.block_table[s0:s1, :sp] == wl.block_table[s0, :sp]).all()
+            used.extend(wl.block_table[s0, :sp].tolist())
     assert len(used) == len(set(used)), "a physical page is shared by two tasks"
     if key == "tiny_extend":
         assert wl.prefix_lens.tolist() == [37, 100, 250, 511]
@@ -73,3 +80,22 @@ def test_determinism_digest():
     h1 = hashlib.sha256(a.q_rows(5, 100, 140).tobytes()).hexdigest()
     h2 = hashlib.sha256(b.q_rows(5, 100, 140).tobytes()).hexdigest()
     assert h1 == h2
+
+
+def test_group_workload_shares_prompt_values():
+    """GRPO groups: every trajectory of a group holds the same K/V on the shared prompt
+    positions (they are the same pages) and its own values after them; Q is per task."""
+    wl = W.make_workload("grpo_group_decode")
+    assert wl.group_start[0] == 0 and wl.group_start[-1] == wl.num_tasks
+    assert (np.diff(wl.group_start) == wl.spec.group_size).all()
+    assert (wl.shared_lens % 16 == 0).all() and (wl.shared_lens >= 2048 - 16).all()
+    for g in (0, 17, 31):
+        s0 = int(wl.group_start[g])
+        sh = int(wl.shared_lens[g])
+        assert (wl.seq_lens[s0:s0 + 8] > sh).all()
+        a = wl.k_rows(s0, sh - 3, sh + 3)
+        b = wl.k_rows(s0 + 5, sh - 3, sh + 3)
+        assert (a[:3] == b[:3]).all() and not (a[3:] == b[3:]).all()
+        va, vb = wl.v_rows(s0 + 1, 0, 20), wl.v_rows(s0 + 7, 0, 20)
+        assert (va == vb).all()
+        assert not (wl.q_rows(s0, 0, 4) == wl.q_rows(s0 + 1, 0, 4)).all()

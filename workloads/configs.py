@@ -16,6 +16,11 @@ shared pool.  The five workloads are:
                      extend U{1024..4096}; K rows x4 on 10% of positions
   long_horizon       32 tasks, 64 q / 8 kv heads, d=128; prefix U{32768..98304},
                      extend U{256..1024}; pool 90% occupied; then 8 decode steps
+  grpo_group_decode  32 GRPO groups x 8 trajectories, 32 q / 8 kv heads, d=128; each
+                     group's prompt (U{2048..6144}, page-aligned) sits in pages all its
+                     trajectories share; each trajectory's own context after it is
+                     lognormal (median 3072, sigma 0.7) clipped to [256, 16384]; one
+                     decoded token each
 
 This module only draws inputs (lengths, page placement, tensor values); it holds
 none of the attention arithmetic.
@@ -57,6 +62,8 @@ class Spec:
     outlier_frac: float = 0.0
     outlier_scale: float = 1.0
     decode_steps: int = 0
+    group_size: int = 0  # > 0: consecutive tasks form GRPO groups sharing a prompt prefix
+    shared: tuple = ()   # group_decode: ("uniform", lo, hi) prompt length, rounded to pages
     salt: int = 0  # 0 for the full-size workload; shrunken variants use their own seeds
 
     @property
@@ -84,7 +91,7 @@ class Spec:
         return dataclasses.replace(
             self, num_tasks=num_tasks, prefix=div_range(self.prefix),
             extend=div_range(self.extend), context=div_range(self.context), pool=pool,
-            salt=salt)
+            shared=div_range(self.shared), salt=salt)
 
 
 SPECS = {
@@ -131,6 +138,17 @@ SPECS = {
         num_tasks=32, num_q_heads=64, num_kv_heads=8, head_dim=128, page_size=16,
         kind="long_horizon", prefix=("uniform", 32 * KILO, 96 * KILO), extend=("uniform", 256, 1024),
         pool=("occupied", 0.9), decode_steps=8),
+    "grpo_group_decode": Spec(
+        key="grpo_group_decode", index=6,
+        text=("GRPO group decode (shared-prompt attention): 32 groups of 8 trajectories, "
+              "32 query / 8 KV heads, head_dim 128, page 16; each group's prompt, uniform "
+              "2k-6k tokens rounded down to whole pages, is stored once in pages every "
+              "trajectory of the group maps; each trajectory's own context after it is "
+              "lognormal (median 3k, sigma 0.7) clipped to [256, 16k]; one decoded token "
+              "per trajectory; bf16 ~ N(0,1)"),
+        num_tasks=256, num_q_heads=32, num_kv_heads=8, head_dim=128, page_size=16,
+        kind="group_decode", context=("lognormal", 3 * KILO, 0.7, 256, 16 * KILO),
+        group_size=8, shared=("uniform", 2 * KILO, 6 * KILO), pool=("fragmented", 1.1)),
 }
 
 
@@ -154,6 +172,8 @@ class Workload:
     num_pages: int
     seeds: dict
     outliers: list = field(default_factory=list)
+    group_start: np.ndarray | None = None  # GRPO groups: tasks group_start[g] .. [g+1]-1
+    shared_lens: np.ndarray | None = None  # positions 0 .. shared-1 in the group's pages
 
     # ---- shape helpers -------------------------------------------------------------
     @property
@@ -183,12 +203,28 @@ class Workload:
         return h.hexdigest()[:16]
 
     # ---- tensor slices (bf16 bit patterns as uint16) --------------------------------
+    def group_of(self, b: int) -> int:
+        return int(np.searchsorted(self.group_start, b, side="right") - 1)
+
     def _rows(self, tensor: int, heads: int, b: int, t0: int, t1: int, out=None) -> np.ndarray:
         d = self.spec.head_dim
         rows = max(0, t1 - t0)
-        flat = None if out is None else out.reshape(-1)
-        flat = _native.normal_bf16(self.seeds[tensor], tensor, b, t0 * heads * d,
-                                   rows * heads * d, out=flat)
+        if out is None:
+            out = np.empty((rows, heads, d), dtype=np.uint16)
+        flat = out.reshape(-1)
+        # K/V of a shared prompt prefix come from the group's own stream (ids after the
+        # tasks'), so every trajectory of the group holds the same values there
+        sh = 0
+        if self.shared_lens is not None and tensor != TENSOR_Q:
+            sh = int(self.shared_lens[self.group_of(b)])
+        cut = min(max(t0, sh), t1)
+        if cut > t0:
+            g = self.num_tasks + self.group_of(b)
+            _native.normal_bf16(self.seeds[tensor], tensor, g, t0 * heads * d,
+                                (cut - t0) * heads * d, out=flat[:(cut - t0) * heads * d])
+        if t1 > cut:
+            _native.normal_bf16(self.seeds[tensor], tensor, b, cut * heads * d,
+                                (t1 - cut) * heads * d, out=flat[(cut - t0) * heads * d:])
         return flat.reshape(rows, heads, d)
 
     def q_rows(self, b: int, t0: int, t1: int, out=None) -> np.ndarray:
@@ -250,6 +286,21 @@ def _f32_to_bf16_exact(f: np.ndarray) -> np.ndarray:
     return (u >> 16).astype(np.uint16)
 
 
+def _draw_group_lengths(spec: Spec, rng: np.random.Generator):
+    """GRPO groups: per-group prompt lengths (whole pages), per-trajectory own context."""
+    b, gsz, ps = spec.num_tasks, spec.group_size, spec.page_size
+    assert b % gsz == 0
+    ng = b // gsz
+    _, lo, hi = spec.shared
+    shared = rng.integers(lo, hi, size=ng, endpoint=True) // ps * ps
+    _, median, sigma, clo, chi = spec.context
+    own = np.clip(np.rint(rng.lognormal(math.log(median), sigma, size=b)), clo, chi)
+    ctx = np.repeat(shared, gsz).astype(np.int64) + own.astype(np.int64)
+    group_start = np.arange(0, b + 1, gsz, dtype=np.int32)
+    # the newest token of each trajectory is the one being decoded: it is appended first
+    return (ctx - 1).astype(np.int32), np.ones(b, dtype=np.int32), group_start, shared.astype(np.int32)
+
+
 def _draw_lengths(spec: Spec, rng: np.random.Generator):
     b = spec.num_tasks
     if spec.kind == "decode":
@@ -277,6 +328,33 @@ def _draw_lengths(spec: Spec, rng: np.random.Generator):
     p = draw(spec.prefix)
     e = draw(spec.extend)
     return p.astype(np.int32), e.astype(np.int32)
+
+
+def _place_group_pages(spec: Spec, prefix, extend, group_start, shared, rng):
+    """Fragmented pool; a group's prompt pages are allocated once and mapped by all of its
+    trajectories, then each trajectory gets its own pages."""
+    ps = spec.page_size
+    final = prefix.astype(np.int64) + extend
+    need = [_ceil_div(int(f), ps) for f in final]
+    stride = max(need)
+    bt = np.full((spec.num_tasks, stride), -1, dtype=np.int32)
+    ng = len(shared)
+    total = sum(int(s) // ps for s in shared) + sum(
+        need[b] - int(shared[g]) // ps for g in range(ng)
+        for b in range(group_start[g], group_start[g + 1]))
+    n = int(math.ceil(spec.pool[1] * total))
+    perm = rng.permutation(n).astype(np.int32)
+    at = 0
+    for g in range(ng):
+        sp = int(shared[g]) // ps
+        pages = perm[at:at + sp]
+        at += sp
+        for b in range(group_start[g], group_start[g + 1]):
+            bt[b, :sp] = pages
+            k = need[b] - sp
+            bt[b, sp:sp + k] = perm[at:at + k]
+            at += k
+    return bt, n
 
 
 def _place_pages(spec: Spec, prefix, extend, rng: np.random.Generator):
@@ -327,8 +405,16 @@ def make_workload(spec: Spec | str) -> Workload:
         spec = SPECS[spec]
     ss = np.random.SeedSequence([2608, 10402, spec.index, spec.salt])
     c_lens, c_pages, c_q, c_k, c_v, c_out = ss.spawn(6)
-    prefix, extend = _draw_lengths(spec, np.random.Generator(np.random.PCG64(c_lens)))
-    bt, n_pages = _place_pages(spec, prefix, extend, np.random.Generator(np.random.PCG64(c_pages)))
+    group_start = shared = None
+    if spec.kind == "group_decode":
+        prefix, extend, group_start, shared = _draw_group_lengths(
+            spec, np.random.Generator(np.random.PCG64(c_lens)))
+        bt, n_pages = _place_group_pages(spec, prefix, extend, group_start, shared,
+                                         np.random.Generator(np.random.PCG64(c_pages)))
+    else:
+        prefix, extend = _draw_lengths(spec, np.random.Generator(np.random.PCG64(c_lens)))
+        bt, n_pages = _place_pages(spec, prefix, extend,
+                                   np.random.Generator(np.random.PCG64(c_pages)))
 
     def seed64(c):
         w = c.generate_state(2, np.uint32)
@@ -341,7 +427,8 @@ def make_workload(spec: Spec | str) -> Workload:
         final = prefix.astype(np.int64) + extend + spec.decode_steps
         outliers = [rng.random(int(f)) < spec.outlier_frac for f in final]
     return Workload(spec=spec, prefix_lens=prefix, extend_lens=extend, block_table=bt,
-                    num_pages=int(n_pages), seeds=seeds, outliers=outliers)
+                    num_pages=int(n_pages), seeds=seeds, outliers=outliers,
+                    group_start=group_start, shared_lens=shared)
 
 
 def custom_workload(num_q_heads: int, num_kv_heads: int, head_dim: int, prefix_lens,
@@ -362,3 +449,35 @@ def custom_workload(num_q_heads: int, num_kv_heads: int, head_dim: int, prefix_l
         if need > num_pages:
             spec = dataclasses.replace(spec, pool=("fragmented", 1.25))
     return make_workload(spec)
+
+
+def custom_group_workload(num_q_heads: int, num_kv_heads: int, head_dim: int, group_sizes,
+                          shared_lens, own_lens, seed: int = 0) -> Workload:
+    """GRPO groups with explicit sizes, shared prompt lengths (page multiples) and each
+    trajectory's own context length after the prompt (>= 1: the decoded token)."""
+    sizes = [int(x) for x in group_sizes]
+    shared = np.asarray(shared_lens, dtype=np.int32)
+    own = np.asarray(own_lens, dtype=np.int64)
+    assert len(shared) == len(sizes) and own.size == sum(sizes) and (own >= 1).all()
+    assert (shared % 16 == 0).all()
+    group_start = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    ctx = np.repeat(shared, sizes).astype(np.int64) + own
+    spec = Spec(key="custom_group", index=200 + seed, text="explicit GRPO groups",
+                num_tasks=int(own.size), num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
+                head_dim=head_dim, page_size=16, kind="group_decode",
+                group_size=max(sizes), pool=("fragmented", 1.25), salt=seed)
+    ss = np.random.SeedSequence([2608, 10402, spec.index, spec.salt])
+    c_lens, c_pages, c_q, c_k, c_v, c_out = ss.spawn(6)
+    prefix = (ctx - 1).astype(np.int32)
+    extend = np.ones(own.size, dtype=np.int32)
+    bt, n_pages = _place_group_pages(spec, prefix, extend, group_start, shared,
+                                     np.random.Generator(np.random.PCG64(c_pages)))
+
+    def seed64(c):
+        w = c.generate_state(2, np.uint32)
+        return int(w[0]) | (int(w[1]) << 32)
+
+    seeds = {TENSOR_Q: seed64(c_q), TENSOR_K: seed64(c_k), TENSOR_V: seed64(c_v)}
+    return Workload(spec=spec, prefix_lens=prefix, extend_lens=extend, block_table=bt,
+                    num_pages=int(n_pages), seeds=seeds, group_start=group_start,
+                    shared_lens=shared)
