@@ -54,6 +54,10 @@ PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
 PROFILE_SUMMARIES = {
     ("agent_resume_7b", "extend"): ("attn_extend_agent_resume_7b_counters.txt", "attn_extend.hip"),
     ("resumed_decode", "decode"): ("decode_split_resumed_decode_counters.txt", "attn_decode.hip"),
+    ("grpo_group_decode", "shared_decode"): ("decode_split_grpo_group_decode_counters.txt",
+                                             "attn_decode.hip"),
+    ("multimodal_prune_resume", "extend"): ("attn_extend_multimodal_prune_resume_counters.txt",
+                                            "attn_extend.hip"),
 }
 
 
@@ -185,7 +189,7 @@ def build_stages(wl, kv, dev, args, torch, np_up):
     ones = np.ones(wl.num_tasks, np.int32)
     stages = []
     keep = {}
-    if s.kind in ("extend", "long_horizon"):
+    if s.kind in ("extend", "long_horizon", "prune_resume"):
         k_ext, v_ext = np_up(wl.packed("k", wl.extend_ranges())), np_up(wl.packed("v", wl.extend_ranges()))
         q_ext = np_up(wl.packed("q", wl.extend_ranges()))
         out_ext = torch.empty_like(q_ext)
@@ -194,7 +198,7 @@ def build_stages(wl, kv, dev, args, torch, np_up):
                             bytes_=append_bytes(wl, int(wl.extend_lens.sum()))))
         stages.append(Stage("extend", lambda: kv.extend(q_ext, wl.prefix_lens, wl.extend_lens, out=out_ext),
                             flops=extend_flops(wl)))
-    if s.kind == "extend":
+    if s.kind in ("extend", "prune_resume"):
         last = np.cumsum(wl.extend_lens) - 1
         q_dec = keep["q_ext"][torch.from_numpy(last.astype(np.int64)).to(dev)].contiguous()
         out_dec = torch.empty_like(q_dec)
@@ -280,6 +284,10 @@ def main():
     elif wl.prefix_lens.sum() > 0:
         kv.append(up(wl.packed("k", wl.prefix_ranges())), up(wl.packed("v", wl.prefix_ranges())),
                   zeros, wl.prefix_lens)
+    if wl.stale_lens is not None:
+        # sliding-window prune: the pages still hold the pre-prune context past the prompt
+        kv.append(up(wl.stale_packed("k")), up(wl.stale_packed("v")), wl.prefix_lens,
+                  (wl.stale_lens - wl.prefix_lens).astype(np.int32))
     stages, keep = build_stages(wl, kv, dev, args, torch, up)
     torch.cuda.synchronize()
     setup_s = time.time() - t_setup

@@ -66,6 +66,13 @@ class DeviceWorkload:
         elif wl.prefix_lens.sum() > 0:
             self.kv.append(dev_bf16(wl.packed("k", wl.prefix_ranges())),
                            dev_bf16(wl.packed("v", wl.prefix_ranges())), zeros, wl.prefix_lens)
+        if wl.stale_lens is not None:
+            # sliding-window prune: the pages still hold the context as it was before the
+            # prune (encoded at the old positions); the resume writes over it
+            n = (wl.stale_lens - wl.prefix_lens).astype(np.int32)
+            if n.sum() > 0:
+                self.kv.append(dev_bf16(wl.stale_packed("k")), dev_bf16(wl.stale_packed("v")),
+                               wl.prefix_lens, n)
 
     def append_extend(self):
         wl = self.wl

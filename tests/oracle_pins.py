@@ -46,12 +46,18 @@ def bits_to_f64(a) -> np.ndarray:
 
 def oracle_pools_for(wl: W.Workload, lib=None, upto: str = "seq"):
     """Oracle pool images holding every position of every task (prefix + extend),
-    built with the oracle's own append: first the prefix rows, then the new rows."""
+    built with the oracle's own append: first the prefix rows, then the new rows.  For a
+    prune resume the pre-prune context is appended after the prefix and before the new
+    rows, which write over its start."""
     hkv, d = wl.spec.num_kv_heads, wl.spec.head_dim
     kp, vp = oracle.new_pools(wl.num_pages, hkv, d)
     zeros = np.zeros_like(wl.prefix_lens)
     oracle.kv_append(wl.packed("k", wl.prefix_ranges()), wl.packed("v", wl.prefix_ranges()),
                      kp, vp, wl.block_table, zeros, wl.prefix_lens, lib=lib)
+    if wl.stale_lens is not None:
+        oracle.kv_append(wl.stale_packed("k"), wl.stale_packed("v"), kp, vp, wl.block_table,
+                         wl.prefix_lens, (wl.stale_lens - wl.prefix_lens).astype(np.int32),
+                         lib=lib)
     oracle.kv_append(wl.packed("k", wl.extend_ranges()), wl.packed("v", wl.extend_ranges()),
                      kp, vp, wl.block_table, wl.prefix_lens, wl.extend_lens, lib=lib)
     return kp, vp
@@ -269,7 +275,7 @@ def pin_append(wl: W.Workload, lib=None):
 
 
 def shrunk_workloads():
-    """CPU-sized versions of the five workloads (same structure, shorter lengths)."""
+    """CPU-sized versions of the workloads (same structure, shorter lengths)."""
     s = W.SPECS
     return [
         W.make_workload(s["tiny_extend"]),
@@ -277,4 +283,5 @@ def shrunk_workloads():
         W.make_workload(s["resumed_decode"].shrunk(num_tasks=6, length_div=32)),
         W.make_workload(s["multimodal_resume"].shrunk(num_tasks=3, length_div=64)),
         W.make_workload(s["long_horizon"].shrunk(num_tasks=2, length_div=256)),
+        W.make_workload(s["multimodal_prune_resume"].shrunk(num_tasks=3, length_div=32)),
     ]

@@ -1,4 +1,4 @@
-"""Full-size parity: the five workloads at their real sizes, in the launch configuration
+"""Full-size parity: the workloads at their real sizes, in the launch configuration
 the benchmark times (automatic work lists and split counts), checked on sampled rows
 that the fp64 oracle recomputes one by one, plus invariants checked on every row.
 
@@ -150,6 +150,47 @@ def test_multimodal_resume_fullsize():
     out, lse = dw.extend()
     _check_extend_rows(wl, out, lse, sample_tasks(wl, 4, seed=7))
     del dw
+    _free()
+
+
+def _check_stale_pages(wl, dw, tasks):
+    """Past the resumed end the pages still hold the pre-prune context, bit for bit."""
+    kp, vp = dw.kv.k_pool, dw.kv.v_pool
+    for b in tasks:
+        n, s = int(wl.seq_lens[b]), int(wl.stale_lens[b])
+        pos = np.arange(n, s)
+        pages = torch.as_tensor(wl.block_table[b, pos // 16].astype(np.int64), device=kp.device)
+        slots = torch.as_tensor(pos % 16, device=kp.device)
+        gk = host_bits(kp[pages, :, slots, :])  # [n, Hkv, d]
+        gv = host_bits(vp[pages, :, :, slots])  # [n, Hkv, d]
+        assert np.array_equal(gk, wl.stale_rows("k", b, n, s)), "task %d stale K" % b
+        assert np.array_equal(gv, wl.stale_rows("v", b, n, s)), "task %d stale V" % b
+
+
+def test_multimodal_prune_resume_fullsize():
+    """Resume after the sliding-window prune: the re-encoded tail is appended over pages
+    holding the pre-prune context, then extend over the prompt; sampled rows against the
+    oracle (which never saw the stale context), the written pages bit for bit, the stale
+    slots past the end untouched, and extend rows equal to the re-prefill's."""
+    wl = W.make_workload("multimodal_prune_resume")
+    log("multimodal_prune_resume: T_ext=%d sumL=%d stale=%d" % (
+        wl.extend_lens.sum(), wl.seq_lens.sum(), wl.stale_lens.sum()))
+    dw = DeviceWorkload(wl)
+    dw.append_extend()
+    out, lse = dw.extend()
+    tasks = sample_tasks(wl, 4, seed=12)
+    _check_extend_rows(wl, out, lse, tasks)
+    _check_append_pages(wl, dw, tasks[:2], lambda b: int(wl.seq_lens[b]))
+    _check_stale_pages(wl, dw, tasks)
+    full, _ = dw.prefill(lse=False)
+    indptr_e = np.concatenate([[0], np.cumsum(wl.extend_lens)])
+    indptr_f = np.concatenate([[0], np.cumsum(wl.seq_lens)])
+    for b in tasks:
+        p, e = int(wl.prefix_lens[b]), int(wl.extend_lens[b])
+        a = out[int(indptr_e[b]):int(indptr_e[b]) + e].float()
+        f = full[int(indptr_f[b]) + p:int(indptr_f[b]) + p + e].float()
+        assert (a - f).abs().max().item() <= 2e-2, b
+    del dw, out, lse, full
     _free()
 
 

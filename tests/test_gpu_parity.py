@@ -1,9 +1,10 @@
 """GPU parity against the fp64 oracle through the C ABI (needs an MI355X).
 
-Sizes: the tiny workload at full size, the four others shrunk so the oracle computes
-every row in seconds while still spanning many 64-key tiles, several token blocks per
-task and ragged page/tile tails; plus explicit edge cases (empty extends, fresh tasks,
-single keys, page and tile boundaries, GQA groups 1..16, head_dim 64 and 128).
+Sizes: the tiny workload at full size, the others shrunk so the oracle computes every
+row in seconds while still spanning many 64-key tiles, several token blocks per task and
+ragged page/tile tails; plus explicit edge cases (empty extends, fresh tasks, single
+keys, page and tile boundaries, GQA groups 1..16, head_dim 64 and 128, resumes written
+over a pruned context).
 """
 import numpy as np
 import pytest
@@ -28,6 +29,15 @@ EXTEND_WORKLOADS = {
     "g4_long": lambda: W.custom_workload(4, 1, 128, [1000], [37], seed=3),
     "g8_outliers": lambda: W.custom_workload(16, 2, 128, [300, 5], [90, 200], seed=4,
                                              outlier_frac=0.1),
+    # sliding-window prune resume: the new rows are written over pages that still hold the
+    # pre-prune context, which must neither leak into the attention nor survive in a
+    # written slot; an empty prompt, page-aligned prompts, a resumed end that lands on a
+    # page boundary (task 3: 64 + 176) and ragged ends inside a stale page
+    "prune_resume_small": lambda: W.make_workload(S["multimodal_prune_resume"].shrunk(4, 16)),
+    "prune_edges_d64": lambda: W.custom_prune_workload(
+        16, 4, 64, [0, 16, 37, 64],
+        [[0] * 10, [3, 40, 0, 7, 1, 12, 33, 2, 9, 5], [5] * 10, [2] + [1] * 9],
+        image_tokens=33, seed=2),
 }
 
 

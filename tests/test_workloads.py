@@ -70,6 +70,40 @@ def test_workload_shapes(key):
     if key == "long_horizon":
         pref_pages = sum(-(-int(p) // 16) for p in wl.prefix_lens)
         assert abs(pref_pages / wl.num_pages - 0.9) < 1e-3
+    if key == "multimodal_prune_resume":
+        images, keep, img, text = s.prune
+        assert (images, keep, img) == (10, 5, 1196)
+        assert wl.prefix_lens.min() >= 512 and wl.prefix_lens.max() <= 2048
+        # the pre-prune context holds ten screenshots and ten texts; the pruned sequence
+        # lost exactly five screenshots and nothing else
+        after = wl.stale_lens - wl.prefix_lens
+        assert (after >= 10 * (img + text[1])).all() and (after <= 10 * (img + text[2])).all()
+        assert ((wl.stale_lens - wl.seq_lens) == 5 * img).all()
+        assert (wl.final_lens == wl.stale_lens).all()
+
+
+def test_prune_rule_on_explicit_turns():
+    """Sliding window (Appendix C): with ten screenshots in context the five oldest are
+    dropped and every turn's text is kept, so the first changed position is the first
+    screenshot, right after the prompt."""
+    texts = [[3] * 10, [0] * 10, list(range(10))]
+    wl = W.custom_prune_workload(8, 2, 64, [0, 16, 37], texts, image_tokens=16, seed=1)
+    assert wl.prefix_lens.tolist() == [0, 16, 37]
+    assert wl.stale_lens.tolist() == [0 + 160 + 30, 16 + 160, 37 + 160 + 45]
+    assert wl.extend_lens.tolist() == [80 + 30, 80, 80 + 45]
+    keep_all = W.custom_prune_workload(8, 2, 64, [20], [[1] * 10], keep=10, image_tokens=16)
+    assert keep_all.extend_lens.tolist() == [0] and keep_all.stale_lens.tolist() == [190]
+
+
+def test_stale_rows_are_their_own_stream():
+    wl = W.make_workload(W.SPECS["multimodal_prune_resume"].shrunk(4, 16))
+    b = 1
+    p, s = int(wl.prefix_lens[b]), int(wl.stale_lens[b])
+    old = wl.stale_rows("k", b, p, s)
+    new = wl.k_rows(b, p, s)
+    assert old.shape == new.shape and (old != new).mean() > 0.9
+    assert np.array_equal(wl.stale_rows("k", b, p + 5, p + 9), old[5:9])
+    assert not np.array_equal(wl.stale_rows("v", b, p, s), old)
 
 
 def test_determinism_digest():

@@ -5,7 +5,7 @@ The paper measures on WebShop, AlfWorld, OSWorld and ScienceBoard trajectories
 Appendix C).  Those datasets are not available here, and the attention path only
 needs their shapes, so every workload below is synthetic: lengths drawn from the
 stated laws, Q/K/V ~ N(0,1) rounded to bf16, and physical pages scattered over a
-shared pool.  The five workloads are:
+shared pool.  The workloads are:
 
   tiny_extend        4 tasks, 8 q / 2 kv heads, d=64; fixed prefix/extend lengths
   agent_resume_7b    64 tasks, 28 q / 4 kv heads (7B-class layer), d=128; prefix
@@ -21,6 +21,13 @@ shared pool.  The five workloads are:
                      trajectories share; each trajectory's own context after it is
                      lognormal (median 3072, sigma 0.7) clipped to [256, 16384]; one
                      decoded token each
+  multimodal_prune_resume
+                     32 tasks, 32 q / 8 kv heads, d=128; prompt U{512..2048}, then ten
+                     turns of (1196-token screenshot, U{64..256} text tokens); the tenth
+                     image prunes the five oldest screenshots, so everything after the
+                     prompt moves: the resume is an extend with P = prompt and E = the
+                     five old turns' text + the five kept turns, written over pages
+                     that still hold the pre-prune context
 
 This module only draws inputs (lengths, page placement, tensor values); it holds
 none of the attention arithmetic.
@@ -62,6 +69,7 @@ class Spec:
     outlier_frac: float = 0.0
     outlier_scale: float = 1.0
     decode_steps: int = 0
+    prune: tuple = ()    # prune_resume: (images, keep, image_tokens, ("uniform", lo, hi) text)
     group_size: int = 0  # > 0: consecutive tasks form GRPO groups sharing a prompt prefix
     shared: tuple = ()   # group_decode: ("uniform", lo, hi) prompt length, rounded to pages
     salt: int = 0  # 0 for the full-size workload; shrunken variants use their own seeds
@@ -88,10 +96,13 @@ class Spec:
         pool = self.pool
         if pool[0] == "perm":
             pool = ("fragmented", 1.5)
+        prune = self.prune
+        if prune:
+            prune = (prune[0], prune[1], max(1, prune[2] // length_div), div_range(prune[3]))
         return dataclasses.replace(
             self, num_tasks=num_tasks, prefix=div_range(self.prefix),
             extend=div_range(self.extend), context=div_range(self.context), pool=pool,
-            shared=div_range(self.shared), salt=salt)
+            shared=div_range(self.shared), prune=prune, salt=salt)
 
 
 SPECS = {
@@ -149,6 +160,18 @@ SPECS = {
         num_tasks=256, num_q_heads=32, num_kv_heads=8, head_dim=128, page_size=16,
         kind="group_decode", context=("lognormal", 3 * KILO, 0.7, 256, 16 * KILO),
         group_size=8, shared=("uniform", 2 * KILO, 6 * KILO), pool=("fragmented", 1.1)),
+    "multimodal_prune_resume": Spec(
+        key="multimodal_prune_resume", index=7,
+        text=("Multi-modal sliding-window prune resume: 32 tasks, 32 query / 8 KV heads, "
+              "head_dim 128, page 16; prompt uniform 512-2048 tokens, then ten turns of one "
+              "1280x720 screenshot (1196 tokens at 28-pixel patches) and uniform 64-256 text "
+              "tokens; on the tenth image the five oldest screenshots are pruned, and the "
+              "resume re-encodes everything after the prompt (the old turns' text and the "
+              "five kept turns) over the pages that held the pre-prune context; also full "
+              "re-prefill of the pruned sequence; bf16 ~ N(0,1)"),
+        num_tasks=32, num_q_heads=32, num_kv_heads=8, head_dim=128, page_size=16,
+        kind="prune_resume", prefix=("uniform", 512, 2048),
+        prune=(10, 5, 1196, ("uniform", 64, 256)), pool=("fragmented", 1.1)),
 }
 
 
@@ -174,6 +197,7 @@ class Workload:
     outliers: list = field(default_factory=list)
     group_start: np.ndarray | None = None  # GRPO groups: tasks group_start[g] .. [g+1]-1
     shared_lens: np.ndarray | None = None  # positions 0 .. shared-1 in the group's pages
+    stale_lens: np.ndarray | None = None   # prune resume: context length before the prune
 
     # ---- shape helpers -------------------------------------------------------------
     @property
@@ -186,7 +210,11 @@ class Workload:
 
     @property
     def final_lens(self) -> np.ndarray:
-        return (self.seq_lens + self.spec.decode_steps).astype(np.int32)
+        """Longest context the task's pages hold at any point (they are mapped up to it)."""
+        n = self.seq_lens.astype(np.int64) + self.spec.decode_steps
+        if self.stale_lens is not None:
+            n = np.maximum(n, self.stale_lens)
+        return n.astype(np.int32)
 
     @property
     def sm_scale(self) -> float:
@@ -226,6 +254,26 @@ class Workload:
             _native.normal_bf16(self.seeds[tensor], tensor, b, cut * heads * d,
                                 (t1 - cut) * heads * d, out=flat[(cut - t0) * heads * d:])
         return flat.reshape(rows, heads, d)
+
+    def stale_rows(self, which: str, b: int, t0: int, t1: int) -> np.ndarray:
+        """K or V the pool held at positions t0..t1-1 before a prune (the pruned and the
+        old, differently encoded turns); drawn from streams of their own."""
+        tensor = {"k": TENSOR_K, "v": TENSOR_V}[which]
+        d, heads = self.spec.head_dim, self.spec.num_kv_heads
+        rows = max(0, t1 - t0)
+        flat = _native.normal_bf16(self.seeds[tensor], tensor, 2 * self.num_tasks + b,
+                                   t0 * heads * d, rows * heads * d)
+        return flat.reshape(rows, heads, d)
+
+    def stale_ranges(self):
+        """Positions that held pre-prune K/V when the resume starts: prompt end .. old end."""
+        return [(int(p), int(s)) for p, s in zip(self.prefix_lens, self.stale_lens)]
+
+    def stale_packed(self, which: str) -> np.ndarray:
+        parts = [self.stale_rows(which, b, t0, t1) for b, (t0, t1) in enumerate(self.stale_ranges())]
+        if not parts:
+            return np.zeros((0, self.spec.num_kv_heads, self.spec.head_dim), np.uint16)
+        return np.concatenate(parts)
 
     def q_rows(self, b: int, t0: int, t1: int, out=None) -> np.ndarray:
         return self._rows(TENSOR_Q, self.spec.num_q_heads, b, t0, t1, out)
@@ -301,6 +349,27 @@ def _draw_group_lengths(spec: Spec, rng: np.random.Generator):
     return (ctx - 1).astype(np.int32), np.ones(b, dtype=np.int32), group_start, shared.astype(np.int32)
 
 
+def _prune_lengths(prompt, texts, images: int, keep: int, image_tokens: int):
+    """Prompt, then turns of (screenshot, text).  With `images` screenshots in context the
+    oldest images - keep are dropped; their turns' text stays.  Returns (P, E, old length):
+    P = position of the first dropped token, E = tokens after it in the pruned sequence."""
+    prompt = np.asarray(prompt, dtype=np.int64)
+    texts = np.asarray(texts, dtype=np.int64).reshape(prompt.size, images)
+    old_len = prompt + images * image_tokens + texts.sum(axis=1)
+    if keep >= images:
+        return prompt.astype(np.int32), np.zeros_like(prompt, np.int32), old_len.astype(np.int32)
+    tail = old_len - prompt - (images - keep) * image_tokens
+    return prompt.astype(np.int32), tail.astype(np.int32), old_len.astype(np.int32)
+
+
+def _draw_prune_lengths(spec: Spec, rng: np.random.Generator):
+    b = spec.num_tasks
+    images, keep, img_tok, text = spec.prune
+    prompt = rng.integers(spec.prefix[1], spec.prefix[2], size=b, endpoint=True)
+    texts = rng.integers(text[1], text[2], size=(b, images), endpoint=True)
+    return _prune_lengths(prompt, texts, images, keep, img_tok)
+
+
 def _draw_lengths(spec: Spec, rng: np.random.Generator):
     b = spec.num_tasks
     if spec.kind == "decode":
@@ -357,9 +426,10 @@ def _place_group_pages(spec: Spec, prefix, extend, group_start, shared, rng):
     return bt, n
 
 
-def _place_pages(spec: Spec, prefix, extend, rng: np.random.Generator):
+def _place_pages(spec: Spec, prefix, extend, rng: np.random.Generator, final=None):
     ps = spec.page_size
-    final = prefix.astype(np.int64) + extend + spec.decode_steps
+    if final is None:
+        final = prefix.astype(np.int64) + extend + spec.decode_steps
     need = [_ceil_div(int(f), ps) for f in final]
     stride = max(1, max(need) if need else 1)
     bt = np.full((spec.num_tasks, stride), -1, dtype=np.int32)
@@ -405,8 +475,15 @@ def make_workload(spec: Spec | str) -> Workload:
         spec = SPECS[spec]
     ss = np.random.SeedSequence([2608, 10402, spec.index, spec.salt])
     c_lens, c_pages, c_q, c_k, c_v, c_out = ss.spawn(6)
-    group_start = shared = None
-    if spec.kind == "group_decode":
+    group_start = shared = stale = None
+    if spec.kind == "prune_resume":
+        prefix, extend, stale = _draw_prune_lengths(spec, np.random.Generator(np.random.PCG64(c_lens)))
+        # the task's pages cover its context before the prune; the resumed sequence reuses
+        # the first of them
+        bt, n_pages = _place_pages(spec, prefix, extend,
+                                   np.random.Generator(np.random.PCG64(c_pages)),
+                                   final=stale.astype(np.int64))
+    elif spec.kind == "group_decode":
         prefix, extend, group_start, shared = _draw_group_lengths(
             spec, np.random.Generator(np.random.PCG64(c_lens)))
         bt, n_pages = _place_group_pages(spec, prefix, extend, group_start, shared,
@@ -428,7 +505,7 @@ def make_workload(spec: Spec | str) -> Workload:
         outliers = [rng.random(int(f)) < spec.outlier_frac for f in final]
     return Workload(spec=spec, prefix_lens=prefix, extend_lens=extend, block_table=bt,
                     num_pages=int(n_pages), seeds=seeds, outliers=outliers,
-                    group_start=group_start, shared_lens=shared)
+                    group_start=group_start, shared_lens=shared, stale_lens=stale)
 
 
 def custom_workload(num_q_heads: int, num_kv_heads: int, head_dim: int, prefix_lens,
@@ -481,3 +558,29 @@ def custom_group_workload(num_q_heads: int, num_kv_heads: int, head_dim: int, gr
     return Workload(spec=spec, prefix_lens=prefix, extend_lens=extend, block_table=bt,
                     num_pages=int(n_pages), seeds=seeds, group_start=group_start,
                     shared_lens=shared)
+
+
+def custom_prune_workload(num_q_heads: int, num_kv_heads: int, head_dim: int, prompt_lens,
+                          texts, images: int = 10, keep: int = 5, image_tokens: int = 1196,
+                          seed: int = 0) -> Workload:
+    """Sliding-window prune resume with explicit prompt lengths and per-turn text lengths
+    (texts[b][i] = text tokens of turn i of task b, `images` turns per task)."""
+    prompt = np.asarray(prompt_lens, dtype=np.int64)
+    prefix, extend, stale = _prune_lengths(prompt, texts, images, keep, image_tokens)
+    spec = Spec(key="custom_prune", index=300 + seed, text="explicit prune resume",
+                num_tasks=int(prompt.size), num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
+                head_dim=head_dim, page_size=16, kind="prune_resume",
+                prune=(images, keep, image_tokens, ("fixed", ())), pool=("fragmented", 1.25),
+                salt=seed)
+    ss = np.random.SeedSequence([2608, 10402, spec.index, spec.salt])
+    c_lens, c_pages, c_q, c_k, c_v, c_out = ss.spawn(6)
+    bt, n_pages = _place_pages(spec, prefix, extend, np.random.Generator(np.random.PCG64(c_pages)),
+                               final=stale.astype(np.int64))
+
+    def seed64(c):
+        w = c.generate_state(2, np.uint32)
+        return int(w[0]) | (int(w[1]) << 32)
+
+    seeds = {TENSOR_Q: seed64(c_q), TENSOR_K: seed64(c_k), TENSOR_V: seed64(c_v)}
+    return Workload(spec=spec, prefix_lens=prefix, extend_lens=extend, block_table=bt,
+                    num_pages=int(n_pages), seeds=seeds, stale_lens=stale)
