@@ -18,6 +18,15 @@ U{2048..16384}, observations log-uniform 64..2048, fragmented page placement):
   grpo_group_decode
     1. KV-append of each trajectory's decoded token, 2. shared-prefix decode
        (tide_decode_attn_shared), 3. plain decode of the same tokens, for comparison
+  multimodal_prune_resume
+    as the extend workloads, with the new rows written over pages that still hold the
+    context from before the sliding-window prune
+  webshop_step (the task-batching scheduler, Section 4)
+    one rollout step of 1056 WebShop-shaped trajectories scheduled round by round by the
+    native scheduler -- Continuous Task Batching, then request-level batching with 1024
+    and 512 tasks in flight -- each round's ops executed by the kernels (append + extend
+    for every (re)prefill, append + decode for every generated token) on one rank's pool
+    of 57344 pages; the step is the whole replay, so --steps and --warmup do not apply
 
 Inputs are resident in HBM before timing starts.  `ms_per_step` comes from HIP events
 around K whole steps on the stream the library launches on.  Each stage is then repeated
@@ -248,6 +257,99 @@ def build_stages(wl, kv, dev, args, torch, np_up):
     return stages, keep
 
 
+CTB_POOL_PAGES = 57344   # 917,504 tokens: a 7B model's KV budget on an 80 GB GPU
+CTB_MAX_RUNNING = 256
+CTB_POLICIES = (("ctb", dict(policy=0)), ("request_f1024", dict(policy=1, max_in_flight=1024)),
+                ("request_f512", dict(policy=1, max_in_flight=512)))
+
+
+def run_ctb(args, torch, tide):
+    """Scheduler workload: replay one rollout step under each policy with the kernels."""
+    import paper_2608_10402_amd.ctb as N
+    import workloads.traces as T
+    tr = T.make_trace(args.workload)
+    s = tr.spec
+    dev = torch.device("cuda", 0)
+    kv = tide.PagedKV(CTB_POOL_PAGES, s.num_q_heads, s.num_kv_heads, s.head_dim,
+                      np.zeros((1, 1), np.int32), device=dev, fill_canary=False)
+    # warm-up: the first rounds of the CTB schedule (kernel loads, workspace growth)
+    warm = N.Scheduler.from_trace(tr, pages_per_rank=CTB_POOL_PAGES, max_running=CTB_MAX_RUNNING)
+    rep = N.Replay(kv, tr.segments)
+    for i, rnd in enumerate(warm.rounds()):
+        rep.run(rnd, timed=False)
+        if i == 60:
+            break
+    warm.close()
+    torch.cuda.synchronize()
+    res = {}
+    for name, cfg in CTB_POLICIES:
+        t0 = time.perf_counter()
+        sched = N.Scheduler.from_trace(tr, pages_per_rank=CTB_POOL_PAGES,
+                                       max_running=CTB_MAX_RUNNING, **cfg)
+        rep = N.Replay(kv, tr.segments)
+        sched_s = 0.0
+        it = sched.rounds()
+        while True:
+            a = time.perf_counter()
+            rnd = next(it, None)
+            sched_s += time.perf_counter() - a
+            if rnd is None:
+                break
+            rep.run(rnd)
+            if rnd.round % 200 == 0:
+                rep.collect()   # bounds the number of live events
+        rep.collect()
+        wall = time.perf_counter() - t0
+        st = sched.stats()
+        sched.close()
+        att = rep.ms["extend"] + rep.ms["decode"]
+        res[name] = {
+            "rounds": st["rounds"], "kv_hit_rate": round(st["hit_tokens"] / st["queried_tokens"], 4),
+            "prefill_tokens": st["extend_tokens"], "recomputed_tokens": st["extend_tokens"] - st["input_tokens"],
+            "pauses": st["pauses"], "extend_ms": round(rep.ms["extend"], 1),
+            "decode_ms": round(rep.ms["decode"], 1), "attention_ms": round(att, 1),
+            "extend_TFLOPs": round(rep.flops / max(rep.ms["extend"], 1e-9) / 1e9, 1),
+            "decode_GBps": round(rep.kv_bytes / max(rep.ms["decode"], 1e-9) / 1e6, 1),
+            "decoded_tokens": rep.tokens["decode"], "replay_wall_s": round(wall, 2),
+            "scheduler_s": round(sched_s, 3), "kernel_calls": rep.calls}
+        print("# %s: %s" % (name, json.dumps(res[name])), file=sys.stderr, flush=True)
+    ctb = res["ctb"]
+    v = ctb["decode_GBps"]
+    roofline = {"bound": "hbm", "achieved": v, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(v / PEAK_HBM_GBS, 4), "kernel": "decode_split_kernel<128, false>",
+                "traffic": None}
+    extra = {"policies": res,
+             "attention_speedup_ctb_vs_request_f1024": round(
+                 res["request_f1024"]["attention_ms"] / ctb["attention_ms"], 3),
+             "attention_speedup_ctb_vs_request_f512": round(
+                 res["request_f512"]["attention_ms"] / ctb["attention_ms"], 3),
+             "hit_rate_gain_vs_request_f1024": round(
+                 ctb["kv_hit_rate"] / res["request_f1024"]["kv_hit_rate"], 3),
+             "hit_rate_gain_vs_request_f512": round(
+                 ctb["kv_hit_rate"] / res["request_f512"]["kv_hit_rate"], 3)}
+    cpu = None
+    if args.cpu_seconds > 0:
+        from oracle import ctb as OC
+        t0 = time.perf_counter()
+        OC.simulate(tr, OC.Config(policy=0, pages_per_rank=CTB_POOL_PAGES,
+                                  max_running=CTB_MAX_RUNNING))
+        dt = time.perf_counter() - t0
+        cpu = {"value": round(ctb["rounds"] / dt, 1), "unit": "scheduled rounds/s", "cores": 1,
+               "kind": "oracle", "sample": "the CTB schedule of the whole trace (%d rounds), "
+               "scheduling only, %.1f s" % (ctb["rounds"], dt)}
+        extra["scheduler_rounds_per_s_native"] = round(ctb["rounds"] / max(ctb["scheduler_s"], 1e-9), 1)
+    line = {
+        "metric": METRIC, "value": v, "unit": "GB/s", "n_gpus": 1, "steps": 1, "warmup": 0,
+        "ms_per_step": ctb["attention_ms"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": s.key, "trajectories": tr.num_tasks, "q_heads": s.num_q_heads,
+                   "kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "page_size": 16,
+                   "pool_pages": CTB_POOL_PAGES, "max_running": CTB_MAX_RUNNING},
+        "roofline": roofline, "cpu_baseline": cpu, "extra": extra}
+    print(json.dumps(line), flush=True)
+    return 0
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -257,6 +359,12 @@ def main():
     import torch
     import paper_2608_10402_amd as tide
     import workloads as W
+    import workloads.traces as WT
+
+    if args.workload in WT.TRACE_SPECS:
+        tide.load()
+        torch.cuda.set_device(0)
+        return run_ctb(args, torch, tide)
 
     tide.load()  # fail loudly if the HIP library is missing
     torch.cuda.set_device(0)

@@ -29,6 +29,7 @@ TIDE_OP_FULL_PREFILL = 4
 
 EXPORTED = ("tide_workspace_size", "tide_kv_append", "tide_extend_attn", "tide_decode_attn",
             "tide_full_prefill_attn", "tide_decode_attn_shared", "tide_workspace_size_shared",
+            "tide_ctb_create", "tide_ctb_step", "tide_ctb_get_stats", "tide_ctb_destroy",
             "tide_status_string", "tide_shutdown")
 
 
@@ -76,6 +77,11 @@ def load(path: str = LIB_PATH):
                                             i32, vp, vp, vp, sz, vp]
     lib.tide_workspace_size_shared.argtypes = [i32, vp, i32, vp, vp, dims_p, i32,
                                                ctypes.POINTER(sz)]
+    lib.tide_ctb_create.argtypes = [vp, i32, vp, vp, i32, vp, vp, vp, vp, vp,
+                                    ctypes.POINTER(vp)]
+    lib.tide_ctb_step.argtypes = [vp, vp]
+    lib.tide_ctb_get_stats.argtypes = [vp, vp]
+    lib.tide_ctb_destroy.argtypes = [vp]
     for name in EXPORTED[:-2]:
         getattr(lib, name).restype = ctypes.c_int
     lib.tide_status_string.argtypes = [ctypes.c_int]

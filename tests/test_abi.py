@@ -16,11 +16,11 @@ import paper_2608_10402_amd as tide
 from paper_2608_10402_amd import _lib
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "tide.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("tide.h", "tide_ctb.h")]
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     return sorted(set(re.findall(r"TIDE_API\s+[\w\s\*]+?\b(tide_\w+)\s*\(", text)))
 
 
@@ -40,7 +40,9 @@ def test_library_exports_exactly_the_header():
 
 
 def test_header_compiles_as_c():
-    src = '#include "tide.h"\nint main(void) { tide_dims d = {8, 2, 64, 16, 0.125f}; (void)d; return 0; }\n'
+    src = ('#include "tide.h"\n#include "tide_ctb.h"\nint main(void) { tide_dims d = {8, 2, 64, 16, '
+           '0.125f}; tide_ctb_config c = {0, 1, 64, 1024, 8, 8, 0, 100}; (void)d; (void)c; '
+           'return 0; }\n')
     r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"),
                         "-x", "c", "-", "-fsyntax-only"], input=src, text=True, capture_output=True)
     assert r.returncode == 0, r.stderr

@@ -1,0 +1,116 @@
+"""The task-batching scheduler driving the kernels on the GPU.
+
+The native scheduler's rounds (already equal to the oracle's, see test_ctb_parity.py)
+are executed by ctb.Replay on one rank's page pool.  Every resume reads K/V that earlier
+rounds wrote into pages the scheduler claims are still valid, so the checks here close
+the loop: sampled extend and decode rows against the fp64 oracle over the trajectory's
+true rows, and the op's pages bit for bit against those rows, for both policies under
+memory pressure (pauses, LRU losses, partial prefix hits).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_10402_amd.ctb as N
+from paper_2608_10402_amd.kvcache import PagedKV
+import workloads.traces as T
+from gpu_harness import assert_close, assert_lse, host_bits, log
+
+pytestmark = pytest.mark.gpu
+
+SPEC = T.TRACE_SPECS["webshop_step"].shrunk(4, 12, 4)
+POOL_PAGES = 1000
+CONFIGS = {
+    "ctb": dict(policy=N.POLICY_CTB, pages_per_rank=POOL_PAGES, max_running=48),
+    "request_f64": dict(policy=N.POLICY_REQUEST, pages_per_rank=POOL_PAGES, max_running=48,
+                        max_in_flight=64),
+}
+
+
+def _oracle_rows(tr, t, positions):
+    """fp64 attention of trajectory t's query rows at `positions` over keys 0..pos, from a
+    compact pool holding only that trajectory (its own append and page order)."""
+    s = tr.spec
+    n = int(max(positions)) + 1
+    n_pages = -(-n // 16)
+    bt = np.random.default_rng(t + 3).permutation(n_pages).astype(np.int32).reshape(1, -1)
+    kp, vp = oracle.new_pools(n_pages, s.num_kv_heads, s.head_dim)
+    oracle.kv_append(tr.rows("k", t, 0, n), tr.rows("v", t, 0, n), kp, vp, bt,
+                     np.array([0], np.int32), np.array([n], np.int32))
+    outs, lses = [], []
+    for p in positions:
+        o, l = oracle.extend(tr.rows("q", t, int(p), int(p) + 1), kp, vp, bt,
+                             np.array([p], np.int32), np.array([1], np.int32), s.num_q_heads,
+                             1.0 / math.sqrt(s.head_dim))
+        outs.append(o[0])
+        lses.append(l[0])
+    return np.stack(outs), np.stack(lses)
+
+
+def _check_pages(kv, tr, t, pages, n):
+    """The op's pages hold trajectory t's K/V for positions 0..n-1, bit for bit."""
+    pg = torch.as_tensor(np.asarray(pages, np.int64), device=kv.device)
+    gk = host_bits(kv.k_pool[pg])                       # [np, Hkv, 16, d]
+    gv = host_bits(kv.v_pool[pg])                       # [np, Hkv, d, 16]
+    pos = np.arange(n)
+    assert np.array_equal(gk[pos // 16, :, pos % 16, :], tr.rows("k", t, 0, n)), t
+    assert np.array_equal(np.transpose(gv, (0, 3, 1, 2))[pos // 16, pos % 16],
+                          tr.rows("v", t, 0, n)), t
+
+
+@pytest.mark.parametrize("name", sorted(CONFIGS))
+def test_replay_against_oracle(name):
+    tr = T.make_trace(SPEC)
+    s = tr.spec
+    sched = N.Scheduler.from_trace(tr, **CONFIGS[name])
+    kv = PagedKV(POOL_PAGES, s.num_q_heads, s.num_kv_heads, s.head_dim,
+                 np.zeros((1, 1), np.int32))
+    rep = N.Replay(kv, tr.segments, with_lse=True)
+    rng = np.random.default_rng(1)
+    got, ref, got_l, ref_l = [], [], [], []
+    n_ext = n_dec = n_resume = n_pages = 0
+    for rnd in sched.rounds():
+        res = rep.run(rnd, timed=False)
+        for kind, (idx, out, lse) in res.items():
+            counts = rnd.ops["count"][idx]
+            first = np.concatenate([[0], np.cumsum(counts)[:-1]])
+            starts = rnd.ops["start"][idx]
+            if kind == "extend":
+                # every resume that reuses a prefix (start > 0), plus some fresh prefills
+                pick = [j for j in range(idx.size) if starts[j] > 0]
+                n_resume += len(pick)
+                pick = pick[:3] + [j for j in range(idx.size) if starts[j] == 0][:1]
+            else:
+                pick = list(rng.choice(idx.size, size=min(2, idx.size), replace=False)) \
+                    if rnd.round % 7 == 0 else []
+            for j in pick:
+                op = rnd.ops[idx[j]]
+                t, st, ct = int(op["task"]), int(op["start"]), int(op["count"])
+                local = sorted({0, ct - 1, int(rng.integers(0, ct))})
+                o, l = _oracle_rows(tr, t, [st + x for x in local])
+                rows = torch.as_tensor([int(first[j]) + x for x in local], device=out.device)
+                got.append(out[rows].float().cpu())
+                got_l.append(lse[rows].cpu())
+                ref.append(o)
+                ref_l.append(l)
+                if kind == "extend":
+                    n_ext += 1
+                else:
+                    n_dec += 1
+                if n_pages < 40:
+                    _check_pages(kv, tr, t, rnd.op_pages(int(idx[j])), st + ct)
+                    n_pages += 1
+    st = sched.stats()
+    log("%s: %d rounds, %d extend / %d decode rows checked, %d prefix-reusing resumes, "
+        "hit rate %.3f, pauses %d" % (name, st["rounds"], n_ext, n_dec, n_resume,
+                                      st["hit_tokens"] / max(1, st["queried_tokens"]),
+                                      st["pauses"]))
+    assert n_ext > 20 and n_dec > 5 and n_resume > 0
+    assert st["extend_tokens"] > st["input_tokens"]  # the pool was small enough to lose KV
+    g = torch.cat(got)
+    assert_close(g, np.concatenate(ref), "%s replay sampled rows" % name)
+    assert_lse(torch.cat(got_l), np.concatenate(ref_l), "%s replay sampled rows" % name)
+    assert rep.tokens["decode"] == int(tr.gen_tokens.sum())

@@ -38,6 +38,10 @@ def _load():
             lib.tg_normal_bf16.restype = None
             lib.tg_normal_f32.argtypes = lib.tg_normal_bf16.argtypes
             lib.tg_normal_f32.restype = None
+            lib.tg_normal_bf16_segments.argtypes = [
+                ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64, ctypes.c_void_p,
+                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
+            lib.tg_normal_bf16_segments.restype = None
             lib.tg_philox4x32_10.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
             lib.tg_philox4x32_10.restype = None
             _lib = lib
@@ -77,4 +81,17 @@ def normal_f32(seed: int, stream_a: int, stream_b: int, first: int, n: int) -> n
     lib = _load()
     out = np.empty(n, dtype=np.float32)
     lib.tg_normal_f32(seed, stream_a, stream_b, first, n, out.ctypes.data, host_threads())
+    return out
+
+
+def normal_bf16_segments(seed: int, stream_a: int, stream_b, first, length) -> np.ndarray:
+    """Concatenation of normal_bf16(seed, stream_a, stream_b[i], first[i], length[i])."""
+    lib = _load()
+    sb = np.ascontiguousarray(stream_b, dtype=np.uint32)
+    fi = np.ascontiguousarray(first, dtype=np.uint64)
+    ln = np.ascontiguousarray(length, dtype=np.int64)
+    assert sb.shape == fi.shape == ln.shape and (ln >= 0).all()
+    out = np.empty(int(ln.sum()), dtype=np.uint16)
+    lib.tg_normal_bf16_segments(seed, stream_a, sb.size, sb.ctypes.data, fi.ctypes.data,
+                                ln.ctypes.data, out.ctypes.data, host_threads())
     return out

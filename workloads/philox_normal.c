@@ -16,6 +16,7 @@
 #define _GNU_SOURCE
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #define PHILOX_M0 0xD2511F53u
@@ -118,4 +119,21 @@ void tg_normal_f32(uint64_t seed, uint32_t sa, uint32_t sb, uint64_t first, int6
       out[e - first] = z[j];
     }
   }
+}
+
+/* Several slices of one tensor family at once: segment i is samples
+   first[i] .. first[i]+len[i]-1 of stream (sa, sb[i]); the segments are written one after
+   another into out.  Used to fetch rows of many tasks in one call. */
+void tg_normal_bf16_segments(uint64_t seed, uint32_t sa, int64_t nseg, const uint32_t* sb,
+                             const uint64_t* first, const int64_t* len, uint16_t* out,
+                             int nthreads) {
+  if (nseg <= 0) return;
+  int64_t* off = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nseg + 1));
+  if (!off) return;
+  off[0] = 0;
+  for (int64_t i = 0; i < nseg; ++i) off[i + 1] = off[i] + len[i];
+#pragma omp parallel for schedule(dynamic, 16) num_threads(nthreads) if (off[nseg] > 65536)
+  for (int64_t i = 0; i < nseg; ++i)
+    tg_normal_bf16(seed, sa, sb[i], first[i], len[i], out + off[i], 1);
+  free(off);
 }
