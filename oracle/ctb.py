@@ -96,6 +96,8 @@ class Pool:
         self.free = deque(range(n))
         self.lru = []               # head (index 0) = least recently released
         self.owner = {}             # page -> (task, logical index), for held and cached pages
+        self.later_free = []        # freed by this round's ops: reusable from the next round
+        self.later_lru = []         # released by this round's ops: evictable from the next round
 
     def alloc(self, task, tasks):
         if self.free:
@@ -116,11 +118,12 @@ class Pool:
         task.pages.append(page)
         return page
 
-    def release(self, task):
+    def release(self, task, later=False):
         """Held pages become cached; the last page is released first, so it is taken
-        first and the longest prefix survives."""
+        first and the longest prefix survives.  `later`: released by an op of the round
+        being executed, so they join the LRU list when the round ends."""
         for p in reversed(task.pages):
-            self.lru.append(p)
+            (self.later_lru if later else self.lru).append(p)
 
     def reclaim(self, task):
         """A task's cached pages become held again."""
@@ -128,12 +131,21 @@ class Pool:
             self.lru.remove(p)
 
     def drop(self, task):
-        """A finished task's pages go back to the free list."""
+        """A finished task's pages go back to the free list when the round ends.  Reading:
+        a round is one batched engine iteration, so no op of the round may rewrite a page
+        another op of the same round reads; pages an op gives up become reusable in the
+        next round (as an engine frees a finished request's blocks after its step)."""
         for p in task.pages:
             del self.owner[p]
-            self.free.append(p)
+            self.later_free.append(p)
         task.pages = []
         task.kv_valid = 0
+
+    def end_round(self):
+        self.free.extend(self.later_free)
+        self.lru.extend(self.later_lru)
+        self.later_free = []
+        self.later_lru = []
 
 
 class Sim:
@@ -334,7 +346,7 @@ class Sim:
             if self.cfg.policy == POLICY_REQUEST:
                 # the turn's request is finished: its pages stay cached, nothing is held
                 self.running[r].remove(t.id)
-                self.pools[r].release(t)
+                self.pools[r].release(t, later=True)
                 t.state = "paused"
 
     # ---------------------------------------------------------------- request policy
@@ -426,6 +438,8 @@ class Sim:
             if after_schedule:
                 after_schedule(self)
             self.execute_request()
+        for pool in self.pools:
+            pool.end_round()
         self.round += 1
         self.stats["rounds"] = self.round
         return self.ops[first:]

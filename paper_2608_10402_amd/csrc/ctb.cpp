@@ -69,6 +69,9 @@ struct Pool {
   std::vector<int32_t> owner_task, owner_idx;
   int32_t head = -1, tail = -1;
   int64_t lru_size = 0;
+  // pages given up by the ops of the round being executed: a round is one batched
+  // engine iteration, so they become reusable (free) or evictable (LRU) when it ends
+  std::vector<int32_t> later_free, later_lru;
 
   explicit Pool(int32_t n)
       : prev(n, -1), next(n, -1), in_lru(n, 0), owner_task(n, -1), owner_idx(n, -1) {
@@ -117,22 +120,30 @@ struct Pool {
     task.pages.push_back(page);
     return page;
   }
-  // Held pages become cached, the last page first.
-  void release(const Task& t) {
-    for (size_t j = t.pages.size(); j-- > 0;) lru_push_back(t.pages[j]);
+  // Held pages become cached, the last page first (at the end of the round if `later`).
+  void release(const Task& t, bool later = false) {
+    for (size_t j = t.pages.size(); j-- > 0;) {
+      if (later) later_lru.push_back(t.pages[j]); else lru_push_back(t.pages[j]);
+    }
   }
   // Cached pages become held again.
   void reclaim(const Task& t) {
     for (int32_t p : t.pages) lru_remove(p);
   }
-  // A finished task's pages return to the free list.
+  // A finished task's pages return to the free list when the round ends.
   void drop(Task& t) {
     for (int32_t p : t.pages) {
       owner_task[p] = owner_idx[p] = -1;
-      free_list.push_back(p);
+      later_free.push_back(p);
     }
     t.pages.clear();
     t.kv_valid = 0;
+  }
+  void end_round() {
+    for (int32_t p : later_free) free_list.push_back(p);
+    for (int32_t p : later_lru) lru_push_back(p);
+    later_free.clear();
+    later_lru.clear();
   }
 };
 
@@ -358,7 +369,7 @@ struct Sim {
       env_due[t.env_done].push_back(t.id);
       if (cfg.policy == TIDE_CTB_POLICY_REQUEST) {
         remove_running(r, t.id);
-        pools[r].release(t);
+        pools[r].release(t, /*later=*/true);
         t.state = State::Paused;
       }
     }
@@ -454,6 +465,7 @@ struct Sim {
       schedule_request();
       execute_request();
     }
+    for (Pool& p : pools) p.end_round();
     ++round;
     stats.rounds = round;
   }

@@ -243,6 +243,11 @@ def _replay_contents(sim, tasks):
     content = {}
     ctx = [0] * len(tasks)
     checked = 0
+    # the ops of one round run as batched kernel calls: no two of them may share a page
+    by_round = {}
+    for rnd, r, kind, t, start, count, pg in sim.ops:
+        for p in pg:
+            assert by_round.setdefault((rnd, r, p), t) == t, (rnd, r, p)
     for rnd, r, kind, t, start, count, pg in sim.ops:
         for pos in range(start):
             assert content.get((r, pg[pos // 16], pos % 16)) == (t, pos), (rnd, t, pos)
@@ -304,3 +309,23 @@ def test_trace_generator_shapes():
     for g in range(len(tr.group_size)):
         firsts = tr.new_tokens[tr.turn_start[:-1][tr.group == g]]
         assert (firsts == firsts[0]).all() and len(firsts) == tr.group_size[g]
+
+
+def test_reusing_a_page_inside_its_round_is_caught(monkeypatch):
+    """Planted mistake: pages an op gives up become reusable within the same round.  The
+    batched execution of a round would then let one op overwrite K/V another op of the
+    round reads; the page-content replay must reject such schedules."""
+    def drop_now(self, task):
+        for p in task.pages:
+            del self.owner[p]
+            self.free.append(p)
+        task.pages = []
+        task.kv_valid = 0
+    release = C.Pool.release
+    monkeypatch.setattr(C.Pool, "drop", drop_now)
+    monkeypatch.setattr(C.Pool, "release", lambda self, task, later=False: release(self, task))
+    rng = random.Random(1)
+    tasks = _random_tasks(rng, 24, 6)
+    sim = _sim(tasks, policy=C.POLICY_CTB, pages_per_rank=40, max_running=6).run()
+    with pytest.raises(AssertionError):
+        _replay_contents(sim, tasks)

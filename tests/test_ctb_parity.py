@@ -155,3 +155,26 @@ def test_native_matches_oracle_on_the_full_webshop_step(cfg):
     tr = T.make_trace("webshop_step")
     cfg = dict(pages_per_rank=57344, max_running=256, **cfg)
     assert _digest_native(tr, **cfg) == _digest_oracle(tr, **cfg)
+
+
+@pytest.mark.parametrize("cfg", [dict(policy=0, pages_per_rank=1000, max_running=48),
+                                 dict(policy=1, pages_per_rank=1000, max_running=48,
+                                      max_in_flight=64)], ids=["ctb", "request_f64"])
+def test_native_rounds_never_share_a_page(cfg):
+    """What the batched GPU replay relies on: the ops of one round touch disjoint pages,
+    and every op's pages hold exactly its own context up to its start."""
+    tr = T.make_trace(T.TRACE_SPECS["webshop_step"].shrunk(4, 12, 4))
+    s = N.Scheduler.from_trace(tr, **cfg)
+    content = {}
+    for r in s.rounds():
+        owner = {}
+        for i, o in enumerate(r.ops):
+            t, st, ct = int(o["task"]), int(o["start"]), int(o["count"])
+            pg = r.op_pages(i)
+            for p in pg:
+                assert owner.setdefault(int(p), t) == t, (r.round, int(p))
+            for pos in range(0, st, 7):
+                assert content.get((int(pg[pos // 16]), pos % 16)) == (t, pos)
+            for pos in range(st, st + ct):
+                content[(int(pg[pos // 16]), pos % 16)] = (t, pos)
+    s.close()
