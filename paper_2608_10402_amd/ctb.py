@@ -154,11 +154,12 @@ class Scheduler:
 class Replay:
     """Runs one rank's scheduled ops on a PagedKV pool with the attention kernels.
 
-    rows(which, tasks, p0, p1) must return the bf16 bit patterns (uint16) of rows
-    p0[i]..p1[i]-1 of every task tasks[i], concatenated: [sum n, heads, d] with heads the
-    query heads for "q" and the KV heads for "k" / "v".  Each round's inputs are uploaded
-    before its kernels are queued, so per-stage events bracket only the library calls
-    (their work-list uploads and kernels).
+    rows(which, tasks, p0, p1) must return rows p0[i]..p1[i]-1 of every task tasks[i],
+    concatenated: [sum n, heads, d] with heads the query heads for "q" and the KV heads
+    for "k" / "v" -- either as a bf16 device tensor, or as bf16 bit patterns (uint16
+    numpy) that are uploaded.  Each round's inputs are ready before its kernels are
+    queued, so per-stage events bracket only the library calls (their work-list uploads
+    and kernels).
     """
 
     def __init__(self, kv: PagedKV, rows, rank: int = 0, with_lse: bool = False):
@@ -180,8 +181,10 @@ class Replay:
             bt[j, : n[j]] = rnd.op_pages(i)
         return bt
 
-    def _up(self, bits: np.ndarray) -> torch.Tensor:
-        t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    def _up(self, rows) -> torch.Tensor:
+        if isinstance(rows, torch.Tensor):
+            return rows
+        t = torch.from_numpy(np.ascontiguousarray(rows).view(np.int16))
         return t.to(self.kv.device).view(torch.bfloat16)
 
     def run(self, rnd: Round, timed: bool = True) -> dict:
