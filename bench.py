@@ -12,7 +12,8 @@ U{2048..16384}, observations log-uniform 64..2048, fragmented page placement):
     4. with --reprefill 1, the recompute a cache miss forces: KV-append of the whole
        history, then full causal re-prefill attention     (tide_kv_append, tide_full_prefill_attn)
   resumed_decode
-    1. KV-append of each task's decoded token, 2. split-K decode over its context
+    1. KV-append of each task's decoded token, 2. split-K decode over its context,
+    3. the same two steps as one fused call (tide_decode_append_attn), for comparison
   long_horizon
     1. KV-append of the new tokens, 2. extend, 3. eight rounds of (append one token, decode)
   grpo_group_decode
@@ -242,6 +243,11 @@ def build_stages(wl, kv, dev, args, torch, np_up):
                             bytes_=append_bytes(wl, wl.num_tasks)))
         stages.append(Stage("decode", lambda: kv.decode(q_dec, wl.seq_lens, out=out_dec),
                             bytes_=decode_bytes(wl, wl.seq_lens)))
+        out_fused = torch.empty_like(q_dec)
+        stages.append(Stage("fused_append_decode",
+                            lambda: kv.decode_append(q_dec, k_new, v_new, wl.seq_lens, out=out_fused),
+                            bytes_=decode_bytes(wl, wl.seq_lens) + append_bytes(wl, wl.num_tasks)))
+        keep.update(out_dec=out_dec, out_fused=out_fused)
     if s.kind == "long_horizon":
         for step in range(s.decode_steps):
             rng = wl.decode_ranges(step)
@@ -496,6 +502,11 @@ def main():
             "flop_ratio_prefill_over_extend": round(prefill_flops(wl) / extend_flops(wl), 3),
             "prefill_tokens_per_s": round(float(wl.seq_lens.sum()) / (ms["prefill"] * 1e-3), 1),
         })
+    if "fused_append_decode" in ms:
+        extra["speedup_fused_vs_append_then_decode"] = round(
+            (ms["append_new"] + ms["decode"]) / ms["fused_append_decode"], 3)
+        extra["fused_vs_separate_bitwise_equal"] = bool(torch.equal(
+            keep["out_dec"].view(torch.int16), keep["out_fused"].view(torch.int16)))
     if any(k.startswith("decode") for k in ms):
         t, _, b = total("decode")
         v = b / (t * 1e-3) / 1e9

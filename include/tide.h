@@ -16,8 +16,10 @@
  *     tide_extend_attn        attention of the new tokens over retained prefix + themselves
  *     tide_decode_attn        one query token per task over its whole context (split-K)
  *     tide_full_prefill_attn  causal attention over the whole sequence (the recompute path)
- *   and one variant of decode for GRPO groups whose trajectories share a prompt prefix:
+ *   and two variants of decode: for GRPO groups whose trajectories share a prompt prefix,
+ *   and with the append of the decoded token fused in:
  *     tide_decode_attn_shared tide_decode_attn, reading each shared prefix once per group
+ *     tide_decode_append_attn tide_kv_append of one token per task + tide_decode_attn
  *
  *   The attention itself is standard scaled dot-product attention (Vaswani et al.,
  *   2017), which the paper uses but does not restate: for a query row at absolute
@@ -169,6 +171,28 @@ TIDE_API int tide_decode_attn(const void* q, const void* k_pool, const void* v_p
                      const int32_t* kv_lens, const tide_dims* dims, int32_t num_splits,
                      void* out, float* lse, void* workspace, size_t workspace_bytes,
                      void* stream);
+
+/*
+ * Decode step with its KV-append fused in: the result and the pool contents afterwards
+ * are those of tide_kv_append(k_new, v_new, prefix_lens = kv_lens - 1, extend_lens = 1)
+ * followed by tide_decode_attn(q, kv_lens).  Every generated token of a resumed task is
+ * such a one-token resume (Section 2.1); fusing removes the append launch and its
+ * round trip through HBM from each step.
+ *   k_new, v_new  bf16 [num_tasks][Hkv][d]: K/V of each task's newest token, which sits
+ *                 at position kv_lens[b] - 1 (its page must be mapped in the block table;
+ *                 its slot is overwritten).
+ * The split that covers that position takes the token straight from k_new / v_new and
+ * writes it into its slot; no other split reads the slot, so there is no ordering
+ * between workgroups.  Workspace: tide_workspace_size(TIDE_OP_DECODE, ...).  Arguments
+ * and errors as tide_decode_attn, plus TIDE_ERR_INVALID_ARG for a NULL k_new / v_new.
+ * In debug mode an invalid page id of the newest token is reported like any other.
+ */
+TIDE_API int tide_decode_append_attn(const void* q, const void* k_new, const void* v_new,
+                            void* k_pool, void* v_pool, int64_t num_pages,
+                            const int32_t* block_table, int32_t bt_stride, int32_t num_tasks,
+                            const int32_t* kv_lens, const tide_dims* dims, int32_t num_splits,
+                            void* out, float* lse, void* workspace, size_t workspace_bytes,
+                            void* stream);
 
 /*
  * Decode attention for tasks grouped by a shared prompt prefix.  GRPO samples a group of

@@ -76,7 +76,11 @@ __device__ __forceinline__ uint2 keep_first4(uint2 x, int n) {
 // kShared: the items are SharedDecodeItem: keys of a prefix shared by ntasks tasks (the
 // MFMA columns are then (task, query head) pairs, ntasks * G <= 16, so every K/V byte is
 // loaded once for all of them), or a task's own keys after it.  Otherwise DecodeItem.
-template <int D, bool kShared>
+// kAppend (plain items only): the newest token of each task (position kv_len - 1) is not
+// in the pool yet.  The split that holds it first writes that token's K/V from
+// a.k_new / a.v_new into its pool slot, waits for the stores, then reads as usual.  No
+// other split reads that slot, so the result equals appending first and then decoding.
+template <int D, bool kShared, bool kAppend>
 __global__ __launch_bounds__(kWavesPerBlock * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void decode_split_kernel(DecodeArgs a) {
   const int lane = threadIdx.x & 63;
@@ -216,6 +220,33 @@ void decode_split_kernel(DecodeArgs a) {
     }
   };
 
+  if constexpr (kAppend) {
+    // The split that ends the context appends its newest token before reading: K row
+    // and V^T column of slot pos % 16, then waits until the stores have completed, so
+    // the loads below return them.  No other wave reads this page (splits end on
+    // 32-key boundaries), and no earlier load in this kernel can have put a stale copy
+    // of it in this CU's L1.
+    if (kend == kv_len) {
+      const int pos = kv_len - 1, slot = pos % kPage;
+      const int32_t p = bt_row[pos / kPage];
+      if (p >= 0 && p < a.num_pages) {
+        const int64_t row = (int64_t)td.row_start * a.num_kv_heads + kv_h;
+        const int64_t blk = ((int64_t)p * a.num_kv_heads + kv_h) * (int64_t)(kPage * D);
+        uint16_t* kdst = const_cast<uint16_t*>(a.k_pool) + blk + (int64_t)slot * D;
+        uint16_t* vdst = const_cast<uint16_t*>(a.v_pool) + blk + slot;
+        const uint16_t* kn = a.k_new + row * D;
+        const uint16_t* vn = a.v_new + row * D;
+        if (lane < D / 8) store_u32x4(kdst + 8 * lane, load_u32x4(kn + 8 * lane));
+#pragma unroll
+        for (int d = lane; d < D; d += 64) vdst[d * kPage] = vn[d];
+      } else {
+        flag_error = true;
+      }
+      __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0) expcnt(0) lgkmcnt(0): stores done
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);  // and no load is moved above them
+    }
+  }
+
   // Two register buffers in ping-pong: the next step is in flight while one is used.
   DecodeRegs<D> ra, rb;
   load(ra, kbeg);
@@ -313,12 +344,12 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_merge_kernel(Decod
   }
 }
 
-template <int D, bool kShared>
+template <int D, bool kShared, bool kAppend>
 hipError_t launch(const DecodeArgs& a, hipStream_t stream) {
   if (a.num_items > 0) {
     const int blocks = (a.num_items + kWavesPerBlock - 1) / kWavesPerBlock;
-    hipLaunchKernelGGL((decode_split_kernel<D, kShared>), dim3(blocks), dim3(kWavesPerBlock * 64),
-                       0, stream, a);
+    hipLaunchKernelGGL((decode_split_kernel<D, kShared, kAppend>), dim3(blocks),
+                       dim3(kWavesPerBlock * 64), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -333,18 +364,26 @@ hipError_t launch(const DecodeArgs& a, hipStream_t stream) {
 
 // Both variants of each head size are instantiated explicitly: the host pass otherwise
 // emits the launch stub of only one of two specialisations that differ in the bool.
-template __global__ void decode_split_kernel<128, false>(DecodeArgs);
-template __global__ void decode_split_kernel<128, true>(DecodeArgs);
-template __global__ void decode_split_kernel<64, false>(DecodeArgs);
-template __global__ void decode_split_kernel<64, true>(DecodeArgs);
+template __global__ void decode_split_kernel<128, false, false>(DecodeArgs);
+template __global__ void decode_split_kernel<128, true, false>(DecodeArgs);
+template __global__ void decode_split_kernel<128, false, true>(DecodeArgs);
+template __global__ void decode_split_kernel<64, false, false>(DecodeArgs);
+template __global__ void decode_split_kernel<64, true, false>(DecodeArgs);
+template __global__ void decode_split_kernel<64, false, true>(DecodeArgs);
 
 }  // namespace kern
 
 hipError_t launch_decode(const DecodeArgs& a, int head_dim, bool shared, hipStream_t stream) {
-  if (head_dim == 128)
-    return shared ? kern::launch<128, true>(a, stream) : kern::launch<128, false>(a, stream);
-  if (head_dim == 64)
-    return shared ? kern::launch<64, true>(a, stream) : kern::launch<64, false>(a, stream);
+  const bool append = a.k_new != nullptr;
+  if (shared && append) return hipErrorInvalidValue;
+  if (head_dim == 128) {
+    if (shared) return kern::launch<128, true, false>(a, stream);
+    return append ? kern::launch<128, false, true>(a, stream) : kern::launch<128, false, false>(a, stream);
+  }
+  if (head_dim == 64) {
+    if (shared) return kern::launch<64, true, false>(a, stream);
+    return append ? kern::launch<64, false, true>(a, stream) : kern::launch<64, false, false>(a, stream);
+  }
   return hipErrorInvalidValue;
 }
 

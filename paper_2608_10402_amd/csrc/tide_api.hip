@@ -296,6 +296,61 @@ TIDE_API int tide_decode_attn(const void* q, const void* k_pool, const void* v_p
     a.out = static_cast<uint16_t*>(out);
     a.lse = lse;
     a.error_flags = at_mut<int32_t>(workspace, 0);
+    a.k_new = nullptr;
+    a.v_new = nullptr;
+    return finish(launch_decode(a, dims->head_dim, false, s), workspace, s);
+  } catch (...) {
+    return TIDE_ERR_HIP;
+  }
+}
+
+TIDE_API int tide_decode_append_attn(const void* q, const void* k_new, const void* v_new,
+                                     void* k_pool, void* v_pool, int64_t num_pages,
+                                     const int32_t* block_table, int32_t bt_stride,
+                                     int32_t num_tasks, const int32_t* kv_lens,
+                                     const tide_dims* dims, int32_t num_splits, void* out,
+                                     float* lse, void* workspace, size_t workspace_bytes,
+                                     void* stream) {
+  try {
+    int rc = check_dims(dims);
+    if (rc != TIDE_OK) return rc;
+    if (num_tasks < 0 || num_splits < 0) return TIDE_ERR_INVALID_ARG;
+    if (num_tasks == 0) return TIDE_OK;
+    if (num_pages <= 0 || bt_stride <= 0) return TIDE_ERR_INVALID_ARG;
+    Plan plan;
+    rc = make_plan(TIDE_OP_DECODE, num_tasks, kv_lens, nullptr, *dims, num_splits, bt_stride,
+                   true, &plan);
+    if (rc != TIDE_OK) return rc;
+    if (!q || !k_new || !v_new || !k_pool || !v_pool || !block_table || !out || !workspace)
+      return TIDE_ERR_INVALID_ARG;
+    if (workspace_bytes < plan.total_bytes) return TIDE_ERR_CAPACITY;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    rc = upload(plan, workspace, s);
+    if (rc != TIDE_OK) return rc;
+    DecodeArgs a;
+    a.q = static_cast<const uint16_t*>(q);
+    a.k_pool = static_cast<const uint16_t*>(k_pool);
+    a.v_pool = static_cast<const uint16_t*>(v_pool);
+    a.block_table = block_table;
+    a.num_pages = num_pages;
+    a.bt_stride = bt_stride;
+    a.num_q_heads = dims->num_q_heads;
+    a.num_kv_heads = dims->num_kv_heads;
+    a.group = dims->num_q_heads / dims->num_kv_heads;
+    a.scale_log2 = dims->sm_scale * 1.44269504088896340736f;
+    a.num_tasks = num_tasks;
+    a.num_items = plan.num_items;
+    a.chunk = plan.chunk;
+    a.max_splits = plan.max_splits;
+    a.tasks = at<TaskDesc>(workspace, plan.tasks_off);
+    a.items = at<DecodeItem>(workspace, plan.items_off);
+    a.part_o = at_mut<float>(workspace, plan.part_o_off);
+    a.part_ml = at_mut<float>(workspace, plan.part_ml_off);
+    a.out = static_cast<uint16_t*>(out);
+    a.lse = lse;
+    a.error_flags = at_mut<int32_t>(workspace, 0);
+    a.k_new = static_cast<const uint16_t*>(k_new);
+    a.v_new = static_cast<const uint16_t*>(v_new);
     return finish(launch_decode(a, dims->head_dim, false, s), workspace, s);
   } catch (...) {
     return TIDE_ERR_HIP;
@@ -366,6 +421,8 @@ TIDE_API int tide_decode_attn_shared(const void* q, const void* k_pool, const vo
     a.out = static_cast<uint16_t*>(out);
     a.lse = lse;
     a.error_flags = at_mut<int32_t>(workspace, 0);
+    a.k_new = nullptr;
+    a.v_new = nullptr;
     return finish(launch_decode(a, dims->head_dim, true, s), workspace, s);
   } catch (...) {
     return TIDE_ERR_HIP;

@@ -126,6 +126,11 @@ struct DecodeArgs {
   uint16_t* out;
   float* lse;
   int32_t* error_flags;
+  // fused append: the K/V rows of each task's newest token (position kv_len - 1),
+  // [num_tasks][Hkv][d]; the split that holds that position writes them into the pool
+  // and uses them directly.  Null for a plain decode.
+  const uint16_t* k_new;
+  const uint16_t* v_new;
 };
 
 }  // namespace tide

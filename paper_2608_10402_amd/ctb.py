@@ -5,7 +5,8 @@ The scheduler (Algorithm 1 of Section 4, or the request-level baseline) is nativ
 in libtide.so; this module marshals its inputs and reads back each round's ops.
 `Replay` then runs those ops on one rank's page pool: for every extend op the new rows
 are appended and attended over the retained prefix (tide_kv_append + tide_extend_attn),
-for every decode op one row is appended and decoded (tide_kv_append + tide_decode_attn).
+for every decode op one row is appended and decoded in one fused call
+(tide_decode_append_attn).
 Row contents come from a caller-supplied function, so the loop holds no model.
 """
 from __future__ import annotations
@@ -212,19 +213,25 @@ class Replay:
             if timed:
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
-                e0.record()
-            ws = kv.workspace(_lib.tide_workspace_size(_lib.TIDE_OP_KV_APPEND, start, count, d))
-            _lib.tide_kv_append(k, v, kv.k_pool, kv.v_pool, bt, start, count, d, ws)
             if kind == OP_EXTEND:
-                ws = kv.workspace(_lib.tide_workspace_size(_lib.TIDE_OP_EXTEND, start, count, d))
+                ws = kv.workspace(max(
+                    _lib.tide_workspace_size(_lib.TIDE_OP_KV_APPEND, start, count, d),
+                    _lib.tide_workspace_size(_lib.TIDE_OP_EXTEND, start, count, d)))
+            else:
+                kv_len = (start + 1).astype(np.int32)
+                ws = kv.workspace(_lib.tide_workspace_size(_lib.TIDE_OP_DECODE, kv_len, None, d))
+            if timed:
+                e0.record()
+            if kind == OP_EXTEND:
+                _lib.tide_kv_append(k, v, kv.k_pool, kv.v_pool, bt, start, count, d, ws)
                 _lib.tide_extend_attn(q, kv.k_pool, kv.v_pool, bt, start, count, d, out, lse, ws)
                 pe = start.astype(np.float64), count.astype(np.float64)
                 self.flops += 4.0 * d.head_dim * d.num_q_heads * float(
                     np.sum(pe[1] * pe[0] + pe[1] * (pe[1] + 1) / 2))
             else:
-                kv_len = (start + 1).astype(np.int32)
-                ws = kv.workspace(_lib.tide_workspace_size(_lib.TIDE_OP_DECODE, kv_len, None, d))
-                _lib.tide_decode_attn(q, kv.k_pool, kv.v_pool, bt, kv_len, d, out, lse, 0, ws)
+                # one token per task: the append is fused into the decode call
+                _lib.tide_decode_append_attn(q, k, v, kv.k_pool, kv.v_pool, bt, kv_len, d, out,
+                                             lse, 0, ws)
                 self.kv_bytes += float(np.sum(kv_len)) * d.num_kv_heads * d.head_dim * 4
             if timed:
                 e1.record()

@@ -74,6 +74,16 @@ class PagedKV:
                               out, lse, num_splits, ws, stream)
         return out
 
+    def decode_append(self, q, k_new, v_new, kv_lens, num_splits: int = 0, out=None, lse=None,
+                      stream=None):
+        """Append each task's newest token (position kv_lens - 1) and decode, fused."""
+        out = torch.empty_like(q) if out is None else out
+        ws = self.workspace(_lib.tide_workspace_size(_lib.TIDE_OP_DECODE, kv_lens, None,
+                                                     self.dims, num_splits))
+        _lib.tide_decode_append_attn(q, k_new, v_new, self.k_pool, self.v_pool, self.block_table,
+                                     kv_lens, self.dims, out, lse, num_splits, ws, stream)
+        return out
+
     def decode_shared(self, q, kv_lens, group_start, shared_lens, num_splits: int = 0, out=None,
                       lse=None, stream=None):
         out = torch.empty_like(q) if out is None else out

@@ -158,6 +158,27 @@ def test_other_entry_points_validation_without_gpu():
                               1 << 20, None) == tide.TIDE_OK              # nothing to append
 
 
+def test_fused_decode_append_validation_without_gpu():
+    lib = tide.load()
+    one = np.array([1], np.int32)
+    bad = np.array([0], np.int32)
+    d = ctypes.byref(GOOD)
+    f = lib.tide_decode_append_attn
+    # (q, k_new, v_new, k_pool, v_pool, num_pages, bt, bt_stride, n, kv_lens, dims, splits,
+    #  out, lse, ws, ws_bytes, stream)
+    assert f(1, 1, 1, 1, 1, 10, 1, 4, 1, bad.ctypes.data, d, 0, 1, None, 1, 1 << 20,
+             None) == tide.TIDE_ERR_INVALID_ARG                            # kv_len 0
+    assert f(1, None, 1, 1, 1, 10, 1, 4, 1, one.ctypes.data, d, 0, 1, None, 1, 1 << 20,
+             None) == tide.TIDE_ERR_INVALID_ARG                            # no k_new
+    assert f(1, 1, None, 1, 1, 10, 1, 4, 1, one.ctypes.data, d, 0, 1, None, 1, 1 << 20,
+             None) == tide.TIDE_ERR_INVALID_ARG                            # no v_new
+    assert f(1, 1, 1, 1, 1, 10, 1, 4, 0, None, d, 0, 1, None, 1, 0, None) == tide.TIDE_OK
+    assert f(1, 1, 1, 1, 1, 10, 1, 4, 1, np.array([65], np.int32).ctypes.data, d, 0, 1, None, 1,
+             1 << 20, None) == tide.TIDE_ERR_CAPACITY                       # 5 pages > 4
+    assert f(1, 1, 1, 1, 1, 10, 1, 4, 1, one.ctypes.data, d, 0, 1, None, 1, 16,
+             None) == tide.TIDE_ERR_CAPACITY                                # workspace too small
+
+
 def test_binding_rejects_host_tensors():
     import torch
     q = torch.zeros(4, 8, 64, dtype=torch.bfloat16)
