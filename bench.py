@@ -540,7 +540,7 @@ def main():
     primary = ("extend" if "extend" in rooflines else
                "shared_decode" if "shared_decode" in rooflines else "decode")
     roofline = dict(rooflines[primary])
-    roofline["kernel"] = {"extend": "extend_attn_kernel<128, false>",
+    roofline["kernel"] = {"extend": "extend_attn_kernel<128, false, false>",
                           "decode": "decode_split_kernel<128, false, false>",
                           "shared_decode": "decode_split_kernel<128, true, false>"}[primary]
     roofline["traffic"] = counter_traffic(s.key, primary)

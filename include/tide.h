@@ -150,6 +150,12 @@ TIDE_API int tide_kv_append(const void* k_new, const void* v_new, void* k_pool, 
  * attend causally to keys 0 .. their own position, read from the pool only: the new
  * tokens' K/V must already have been appended.  q/out rows are packed by extend_lens.
  * extend_lens[b] == 0 contributes no rows; prefix_lens[b] == 0 is a fresh prefill.
+ * A call with too few (task, kv head, token block) work items to keep every compute
+ * unit busy is run split-KV: long blocks are cut into key ranges processed in parallel
+ * and merged by a second kernel (the workspace then also holds the fp32 partials).  The
+ * choice depends only on the lengths and dims, so tide_workspace_size covers it and
+ * results stay bitwise repeatable; the environment variable TIDE_EXTEND_SPLIT=0 (never)
+ * or =1 (whenever a block spans enough key tiles) overrides it, read on every call.
  */
 TIDE_API int tide_extend_attn(const void* q, const void* k_pool, const void* v_pool, int64_t num_pages,
                      const int32_t* block_table, int32_t bt_stride, int32_t num_tasks,

@@ -277,71 +277,14 @@ void decode_split_kernel(DecodeArgs a) {
   }
 }
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, xor_shfl(v, m));
-  return v;
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += xor_shfl(v, m);
-  return v;
-}
-
-// One wave per (task, query head): combine the task's split partials.  Lane s owns split
-// s for the statistics (max, weights); the partial outputs are then accumulated with
-// every lane covering D/64 head-dim entries and the weights broadcast across the wave.
+// One wave per (task, query head): combine the task's split partials.
 template <int D>
 __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_merge_kernel(DecodeArgs a) {
-  const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
   if (row >= (int64_t)a.num_tasks * a.num_q_heads) return;
   const int task = (int)(row / a.num_q_heads);
-  const int nsplit = a.tasks[task].aux;
-  const float* ml = a.part_ml + row * a.max_splits * 4;
-  const float* po = a.part_o + row * a.max_splits * D;
-  constexpr int kPer = D / 64;
-
-  float mx = kNoMax;
-  for (int s = lane; s < nsplit; s += 64) mx = fmaxf(mx, ml[4 * s]);
-  mx = wave_max(mx);
-
-  float acc[kPer];
-#pragma unroll
-  for (int i = 0; i < kPer; ++i) acc[i] = 0.0f;
-  float l_round = 0.0f, l_ex = 0.0f;
-  for (int s0 = 0; s0 < nsplit; s0 += 64) {
-    const int s = s0 + lane;
-    float wgt = 0.0f;
-    if (s < nsplit) {
-      const f32x4 st = *reinterpret_cast<const f32x4*>(ml + 4 * s);
-      wgt = fast_exp2(st[0] - mx);
-      l_round += wgt * st[1];
-      l_ex += wgt * st[2];
-    }
-    const int n = min(64, nsplit - s0);
-#pragma unroll 4
-    for (int i = 0; i < n; ++i) {
-      const float wi = __shfl(wgt, i, 64);
-      const float* src = po + (int64_t)(s0 + i) * D + kPer * lane;
-#pragma unroll
-      for (int k = 0; k < kPer; ++k) acc[k] += wi * src[k];
-    }
-  }
-  l_round = wave_sum(l_round);
-  const float inv = 1.0f / l_round;
-  uint16_t* orow = a.out + row * D;
-  if (kPer == 2) {
-    *reinterpret_cast<uint32_t*>(orow + 2 * lane) = pack_bf16x2(acc[0] * inv, acc[kPer - 1] * inv);
-  } else {
-    const uint32_t w = pack_bf16x2(acc[0] * inv, 0.0f);
-    orow[lane] = (uint16_t)(w & 0xFFFFu);
-  }
-  if (a.lse) {
-    l_ex = wave_sum(l_ex);
-    if (lane == 0) a.lse[row] = (mx + __log2f(l_ex)) * kLn2;
-  }
+  merge_partials<D>(a.part_ml + row * a.max_splits * 4, 4, a.part_o + row * a.max_splits * D, D,
+                    a.tasks[task].aux, a.out + row * D, a.lse ? a.lse + row : nullptr);
 }
 
 template <int D, bool kShared, bool kAppend>

@@ -131,7 +131,11 @@ __device__ __forceinline__ float pair_sum(float v) {
 // kLse: also keep the exact fp32 sum of the probabilities, so the returned log-sum-exp is
 // the true one; the output itself is normalised by the sum of the bf16-rounded weights
 // that the P.V product used.
-template <int D, bool kLse>
+// kSplit: the work list is the split-KV plan's.  A workgroup walks the key tiles
+// [t_begin, t_end) of its item; a chunk of a split item writes its unnormalised fp32
+// output and statistics to the partial buffers for extend_merge_kernel, an unsplit item
+// writes its rows as usual.
+template <int D, bool kLse, bool kSplit>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void extend_attn_kernel(ExtendArgs a) {
   using S = ES<D>;
@@ -152,7 +156,18 @@ void extend_attn_kernel(ExtendArgs a) {
   const int pw = wave & 3;        // page of every tile this wave fetches
   const int q = lane & 31, h = lane >> 5;
 
-  const ExtendItem it = a.items[blockIdx.x];
+  ExtendItem it;
+  int tbase = 0, split = -1, pbase = 0, t_stop = 0;
+  if constexpr (kSplit) {
+    const ExtendChunkItem ci = a.chunk_items[blockIdx.x];
+    it = ExtendItem{ci.task, ci.kv_head, ci.tok0, ci.ntok};
+    tbase = ci.t_begin;
+    t_stop = ci.t_end;
+    split = ci.split;
+    pbase = ci.pbase;
+  } else {
+    it = a.items[blockIdx.x];
+  }
   if (it.ntok == 0) return;  // padding slot of the XCD-interleaved work list
   const TaskDesc td = a.tasks[it.task];
   const int P = td.prefix;
@@ -160,7 +175,9 @@ void extend_attn_kernel(ExtendArgs a) {
   const int G = a.group;
   const int npages = (seq_len + kPage - 1) / kPage;
   const int kend = P + it.tok0 + it.ntok;     // keys needed by the last row
-  const int ntiles = (kend + 63) / 64;
+  // Tiles walked, counted from tile tbase: below, `tile` is this local index (it picks
+  // the LDS buffers) and tbase + tile the key tile (64 keys from key 0).
+  const int ntiles = kSplit ? t_stop - tbase : (kend + 63) / 64;
   const int n_full = (P + it.tok0 + 1) / 64;  // tiles every row sees completely
 
   // ---- K/V streaming: waves 0-3 fetch the K pages, waves 4-7 the V^T pages ---------
@@ -179,7 +196,7 @@ void extend_attn_kernel(ExtendArgs a) {
   // Page id of this wave's page of `tile` (a scalar load); pages past the sequence are
   // read from page 0, which always exists: their keys are masked, their V zeroed.
   auto page_word = [&](int tile) -> int32_t {
-    const int lp = tile * 4 + pw;
+    const int lp = (tbase + tile) * 4 + pw;
     return lp < npages ? load_page_id(bt, lp) : 0;
   };
   // Every step issues the same number of loads on every wave, so the vmcnt waits below
@@ -236,9 +253,9 @@ void extend_attn_kernel(ExtendArgs a) {
   f32x16 s[2];
   u32x4 pb[4];  // bf16 probabilities of the last softmaxed tile, one 16-key chunk each
 
-  // O^T += V^T.P^T for `tile`, V^T in vb.  With kTail, the V slots of keys at or beyond
-  // seq_len are zeroed in registers (0 * NaN would otherwise poison O); only an item's
-  // last tile can hold such keys.
+  // O^T += V^T.P^T for key tile `tile`, V^T in vb.  With kTail, the V slots of keys at or
+  // beyond seq_len are zeroed in registers (0 * NaN would otherwise poison O); only the
+  // last tile a workgroup walks can hold such keys.
   auto pv = [&](const uint8_t* vb, int tile, auto tail_tag) {
     constexpr bool kTail = decltype(tail_tag)::value;
 #pragma unroll
@@ -291,8 +308,9 @@ void extend_attn_kernel(ExtendArgs a) {
   // (v_exp_f32, which does not overlap MFMAs on the same SIMD).  o2: bf16 packing into
   // pb and the row sums.
   auto softmax_o1 = [&](int tile) {
-    if (tile >= n_full) {  // diagonal / tail tile: hide keys past this row's position
-      const int kbase = tile * 64 + 8 * h;
+    const int kt = tbase + tile;
+    if (kt >= n_full) {  // diagonal / tail tile: hide keys past this row's position
+      const int kbase = kt * 64 + 8 * h;
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
@@ -358,7 +376,7 @@ void extend_attn_kernel(ExtendArgs a) {
   // is in LDS before the next round starts.
   auto step = [&](int tile, uint8_t* kv, uint8_t* kv_prev) {
     if (tile > 0) {
-      pv(kv_prev + S::kTileBytes, tile - 1, std::false_type());
+      pv(kv_prev + S::kTileBytes, tbase + tile - 1, std::false_type());
       qk(kv);
       pipeline(std::integral_constant<int, 4 * kDT + 2 * kDC>());
     } else {
@@ -393,17 +411,42 @@ void extend_attn_kernel(ExtendArgs a) {
       if (tile + 2 < ntiles) step(tile + 2, kv_lds2, kv_lds1);
     }
   }
+  const int last = tbase + ntiles - 1;
   switch ((ntiles - 1) & 3) {  // P.V of the last tile
-    case 0: pv(kv_lds0 + S::kTileBytes, ntiles - 1, std::true_type()); break;
-    case 1: pv(kv_lds1 + S::kTileBytes, ntiles - 1, std::true_type()); break;
-    case 2: pv(kv_lds2 + S::kTileBytes, ntiles - 1, std::true_type()); break;
-    default: pv(kv_lds3 + S::kTileBytes, ntiles - 1, std::true_type()); break;
+    case 0: pv(kv_lds0 + S::kTileBytes, last, std::true_type()); break;
+    case 1: pv(kv_lds1 + S::kTileBytes, last, std::true_type()); break;
+    case 2: pv(kv_lds2 + S::kTileBytes, last, std::true_type()); break;
+    default: pv(kv_lds3 + S::kTileBytes, last, std::true_type()); break;
   }
   if (!v_half) phase_barrier();  // balances the offset barrier of waves 4-7
   wait_vmem<0>();  // no transfer into LDS may outlive the workgroup
 
   if (bad_page && lane == 0) atomicOr(a.error_flags, 1);
   const float l_tot = pair_sum(l_part);
+  if (kSplit && split >= 0) {
+    // Lanes l and l^32 hold the same row, so both take this branch or neither.
+    const float l_ex = kLse ? pair_sum(l_exact) : 0.0f;
+    if (row_valid) {
+      const int64_t slot =
+          (int64_t)(pbase + split * it.ntok + tk) * a.num_q_heads + it.kv_head * G + j;
+      float* po = a.part_o + slot * D;
+#pragma unroll
+      for (int t = 0; t < kDT; ++t)
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const f32x4 w0 = {o[t][8 * half], o[t][8 * half + 1], o[t][8 * half + 2], o[t][8 * half + 3]};
+          const f32x4 w1 = {o[t][8 * half + 4], o[t][8 * half + 5], o[t][8 * half + 6],
+                            o[t][8 * half + 7]};
+          *reinterpret_cast<f32x4*>(po + 32 * t + 16 * half + 8 * h) = w0;
+          *reinterpret_cast<f32x4*>(po + 32 * t + 16 * half + 8 * h + 4) = w1;
+        }
+      if (h == 0) {
+        const f32x4 ml = {m_ref, l_tot, l_ex, 0.0f};
+        *reinterpret_cast<f32x4*>(a.part_ml + slot * 4) = ml;
+      }
+    }
+    return;
+  }
   if (row_valid) {
     const float inv = 1.0f / l_tot;
     uint16_t* orow = a.out + qrow * D;
@@ -424,21 +467,56 @@ void extend_attn_kernel(ExtendArgs a) {
   }
 }
 
+constexpr int kMergeWaves = 4;
+
+// One wave per (packed row, query head) of a split-KV call: combines the row's chunk
+// partials; rows that were not split were written by the attention kernel.
 template <int D>
-hipError_t launch(const ExtendArgs& a, hipStream_t stream) {
+__global__ __launch_bounds__(kMergeWaves * 64) void extend_merge_kernel(ExtendArgs a) {
+  const int64_t w = (int64_t)blockIdx.x * kMergeWaves + (threadIdx.x >> 6);
+  if (w >= (int64_t)a.total_rows * a.num_q_heads) return;
+  const int row = (int)(w / a.num_q_heads);
+  const int head = (int)(w - (int64_t)row * a.num_q_heads);
+  const MergeRow mr = a.merge_rows[row];
+  if (mr.nsplit == 0) return;
+  const int64_t s0 = (int64_t)mr.base * a.num_q_heads + head;
+  const int64_t ss = (int64_t)mr.stride * a.num_q_heads;
+  merge_partials<D>(a.part_ml + s0 * 4, ss * 4, a.part_o + s0 * D, ss * D, mr.nsplit,
+                    a.out + w * D, a.lse ? a.lse + w : nullptr);
+}
+
+template <int D, bool kSplit>
+hipError_t launch_attn(const ExtendArgs& a, hipStream_t stream) {
   if (a.lse)
-    hipLaunchKernelGGL((extend_attn_kernel<D, true>), dim3(a.num_items), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((extend_attn_kernel<D, true, kSplit>), dim3(a.num_items), dim3(kThreads), 0,
+                       stream, a);
   else
-    hipLaunchKernelGGL((extend_attn_kernel<D, false>), dim3(a.num_items), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((extend_attn_kernel<D, false, kSplit>), dim3(a.num_items), dim3(kThreads), 0,
+                       stream, a);
   return hipGetLastError();
 }
 
-// Both variants of each head size are instantiated explicitly: the host pass otherwise
-// emits the launch stub of only one of two specialisations that differ in the bool.
-template __global__ void extend_attn_kernel<128, false>(ExtendArgs);
-template __global__ void extend_attn_kernel<128, true>(ExtendArgs);
-template __global__ void extend_attn_kernel<64, false>(ExtendArgs);
-template __global__ void extend_attn_kernel<64, true>(ExtendArgs);
+template <int D>
+hipError_t launch(const ExtendArgs& a, hipStream_t stream) {
+  if (!a.chunk_items) return launch_attn<D, false>(a, stream);
+  hipError_t e = launch_attn<D, true>(a, stream);
+  if (e != hipSuccess || !a.merge_rows) return e;
+  const int64_t waves = (int64_t)a.total_rows * a.num_q_heads;
+  const int blocks = (int)((waves + kMergeWaves - 1) / kMergeWaves);
+  hipLaunchKernelGGL((extend_merge_kernel<D>), dim3(blocks), dim3(kMergeWaves * 64), 0, stream, a);
+  return hipGetLastError();
+}
+
+// Every variant is instantiated explicitly: the host pass otherwise emits the launch stub
+// of only one of the specialisations that differ in a bool.
+template __global__ void extend_attn_kernel<128, false, false>(ExtendArgs);
+template __global__ void extend_attn_kernel<128, true, false>(ExtendArgs);
+template __global__ void extend_attn_kernel<64, false, false>(ExtendArgs);
+template __global__ void extend_attn_kernel<64, true, false>(ExtendArgs);
+template __global__ void extend_attn_kernel<128, false, true>(ExtendArgs);
+template __global__ void extend_attn_kernel<128, true, true>(ExtendArgs);
+template __global__ void extend_attn_kernel<64, false, true>(ExtendArgs);
+template __global__ void extend_attn_kernel<64, true, true>(ExtendArgs);
 
 }  // namespace kern
 

@@ -2,6 +2,7 @@
 #include "plan.h"
 
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -61,6 +62,290 @@ int task_lengths(int op, int32_t b, const int32_t* lens_a, const int32_t* lens_b
 
 }  // namespace
 
+// ---- extend / prefill work lists ------------------------------------------------------
+//
+// A work item is one block of tb = 256 / G tokens of one (task, kv head): its 256 query
+// rows are the block's (token, head) pairs, and one 8-wave workgroup, which fills a CU,
+// walks the key tiles (64 keys) the block sees.  Two plans are considered:
+//   plain  every item walks all its tiles and writes its rows;
+//   split  a block that spans many tiles is cut into chunks of about T tiles that run on
+//          different CUs and write unnormalised fp32 partials, which a second kernel
+//          merges (the split-K scheme of flash decoding, applied to extend blocks).
+// Splitting pays when a call has too few items to keep 256 CUs busy to the end.  The
+// choice compares closed-form run-time estimates: the makespan of n workgroups costing
+// c_i tiles each on 256 CUs is taken as max(max c, sum c / 256 + max c / 2), a tile costs
+// less while few CUs are busy (the clock is higher), and a split plan adds the merge's
+// HBM traffic and launch.  The planner runs on every call, so everything here is linear
+// in the number of blocks, and only the chosen plan is materialised.
+namespace {
+
+constexpr int kCus = 256;  // MI355X compute units, 32 per XCD
+// Cost model, in units of one key tile of one workgroup at full occupancy; the overheads
+// and rates were fitted to measured one- to 64-task calls (GQA 28/4, d = 128).
+constexpr double kItemOverhead = 0.5;     // first-tile latency and epilogue
+constexpr double kChunkOverhead = 2.5;    // the same plus the fp32 partial write
+constexpr double kCuFlopsPerUs = 3.9e6;   // sustained MFMA rate of one CU, all CUs busy
+constexpr double kIdleClockGain = 0.25;   // a tile is up to this much cheaper with idle CUs
+constexpr double kHbmBytesPerUs = 5.0e6;  // sustained HBM rate of the merge
+constexpr double kMergeLaunchUs = 4.0;    // second kernel launch
+constexpr double kSplitGain = 1.0;        // split whenever estimated faster
+constexpr int kMinChunkTiles = 8;
+constexpr int kMaxChunks = 512;
+constexpr int64_t kSplitMaxItems = 2048;  // larger calls fill the chip with the plain plan
+
+struct Block {
+  int32_t task, tok0, ntok, ntiles;
+};
+
+// Chunks of a block for chunk length T: about ntiles / T, on a fixed grid [c*T, (c+1)*T)
+// whose last chunk takes the rest (up to 1.5 T), so the same chunk of a unit's blocks
+// covers the same keys.  T == 0: the plain plan (one chunk).
+inline int32_t num_chunks(int32_t ntiles, int32_t T) {
+  if (T <= 0) return 1;
+  return (int32_t)std::min<int64_t>(kMaxChunks, std::max<int64_t>(1, (ntiles + T / 2) / T));
+}
+
+inline int32_t chunk_tiles(int32_t ntiles, int32_t T, int32_t n, int32_t c) {
+  return c == n - 1 ? ntiles - c * T : T;
+}
+
+inline double chunk_cost(int32_t ntiles, int32_t T, int32_t n, int32_t c) {
+  return chunk_tiles(ntiles, T, n, c) + (n > 1 ? kChunkOverhead : kItemOverhead);
+}
+
+// Estimated run time (us) of the plan with chunk length T (0: plain).
+double estimate(const std::vector<Block>& blocks, int32_t num_kv_heads, int32_t num_q_heads,
+                int32_t head_dim, int32_t T, double tile_us, int64_t* row_slots) {
+  double total = 0.0, biggest = 0.0;
+  int64_t items = 0, slots = 0;
+  for (const Block& b : blocks) {
+    const int32_t n = num_chunks(b.ntiles, T);
+    items += n;
+    if (n > 1) slots += (int64_t)b.ntok * n;
+    total += (n - 1) * chunk_cost(b.ntiles, T, n, 0) + chunk_cost(b.ntiles, T, n, n - 1);
+    for (int32_t c : {0, n - 1}) biggest = std::max(biggest, chunk_cost(b.ntiles, T, n, c));
+  }
+  items *= num_kv_heads;
+  total *= num_kv_heads;
+  const double busy = std::min(1.0, (double)items / kCus);
+  const double t_eff = tile_us * (1.0 - kIdleClockGain * (1.0 - busy));
+  double us = std::max(biggest, total / kCus + 0.5 * biggest) * t_eff;
+  if (slots > 0)
+    us += (double)slots * num_q_heads * (head_dim * 4.0 + 16.0) * 2.0 / kHbmBytesPerUs +
+          kMergeLaunchUs;
+  *row_slots = slots;
+  return us;
+}
+
+// Consecutive blocks [k0, k1) of one task (longest first), chunk c (-1: whole blocks)
+// of kv head g.  Workgroups of a piece read the same K/V.
+struct Piece {
+  double cost;
+  int32_t k0, k1, g, c;
+};
+
+// Item order.  Workgroups are dispatched round-robin over the XCDs (slot i runs on XCD
+// i % 8), each with its own L2.  A column -- one (task, kv head, chunk) -- is kept on one
+// XCD, its items consecutive, so workgroups that walk the same K/V run side by side and
+// share it through L2 instead of re-reading HBM.  A column longer than a quarter of an
+// XCD's share is cut into consecutive pieces first, so that a call with fewer units than
+// XCDs still reaches every XCD; pieces then go longest first to the least loaded XCD.
+// Returns, per XCD, its pieces in order.
+std::vector<std::vector<Piece>> place(const std::vector<Block>& blocks,
+                                      const std::vector<int32_t>& task_first,
+                                      const std::vector<int32_t>& nchunks, int32_t num_kv_heads,
+                                      int32_t T) {
+  const int32_t ntasks = (int32_t)task_first.size() - 1;
+  std::vector<Piece> cols;
+  double total = 0.0, biggest = 0.0;
+  for (int32_t b = 0; b < ntasks; ++b) {
+    const int32_t k0 = task_first[b], k1 = task_first[b + 1];
+    if (k0 == k1) continue;
+    const int32_t nmax = nchunks[k0];  // chunk counts do not grow along a task's blocks
+    for (int32_t c = 0; c < nmax; ++c) {
+      int32_t end = k0;
+      double cost = 0.0;
+      while (end < k1 && nchunks[end] > c) {
+        const double ci = chunk_cost(blocks[end].ntiles, T, nchunks[end], c);
+        cost += ci;
+        biggest = std::max(biggest, ci);
+        ++end;
+      }
+      for (int32_t g = 0; g < num_kv_heads; ++g)
+        cols.push_back(Piece{cost, k0, end, g, T > 0 ? c : -1});
+      total += cost * num_kv_heads;
+    }
+  }
+  const double cap = std::max(biggest, total / (kXcds * 4));
+  std::vector<Piece> pieces;
+  pieces.reserve(cols.size());
+  for (const Piece& col : cols) {
+    const int32_t c = std::max(col.c, 0);
+    Piece cur{0.0, col.k0, col.k0, col.g, col.c};
+    for (int32_t k = col.k0; k < col.k1; ++k) {
+      const double ci = chunk_cost(blocks[k].ntiles, T, nchunks[k], c);
+      if (cur.k1 > cur.k0 && cur.cost + ci > cap) {
+        pieces.push_back(cur);
+        cur = Piece{0.0, k, k, col.g, col.c};
+      }
+      cur.k1 = k + 1;
+      cur.cost += ci;
+    }
+    if (cur.k1 > cur.k0) pieces.push_back(cur);
+  }
+  std::stable_sort(pieces.begin(), pieces.end(),
+                   [](const Piece& x, const Piece& y) { return x.cost > y.cost; });
+  std::vector<std::vector<Piece>> queues(kXcds);
+  double load[kXcds] = {};
+  for (const Piece& p : pieces) {
+    const int x = (int)(std::min_element(load, load + kXcds) - load);
+    load[x] += p.cost;
+    queues[x].push_back(p);
+  }
+  return queues;
+}
+
+// Item slots in dispatch order: slot i * 8 + x is the i-th item of XCD x's queue, and an
+// XCD whose queue ran out gets empty slots (ntok == 0) that return at once.
+template <class Item, class Make>
+std::vector<Item> interleave(const std::vector<std::vector<Piece>>& queues, Make make) {
+  std::vector<std::vector<Item>> per(kXcds);
+  size_t depth = 0;
+  for (int x = 0; x < kXcds; ++x) {
+    for (const Piece& p : queues[x])
+      for (int32_t k = p.k0; k < p.k1; ++k) per[x].push_back(make(k, p.g, std::max(p.c, 0)));
+    depth = std::max(depth, per[x].size());
+  }
+  std::vector<Item> items(depth * kXcds);  // value-initialised: ntok == 0
+  for (int x = 0; x < kXcds; ++x)
+    for (size_t i = 0; i < per[x].size(); ++i) items[i * kXcds + x] = per[x][i];
+  while (!items.empty() && items.back().ntok == 0) items.pop_back();
+  return items;
+}
+
+template <class Item>
+void to_bytes(const std::vector<Item>& v, std::vector<uint8_t>* out) {
+  out->resize(v.size() * sizeof(Item));
+  if (!v.empty()) memcpy(out->data(), v.data(), out->size());
+}
+
+int plan_extend(const std::vector<TaskDesc>& tasks, const tide_dims& dims, bool build_blob,
+                Plan* plan, std::vector<uint8_t>* items_bytes, std::vector<uint8_t>* merge_bytes,
+                int64_t* n_items) {
+  const int32_t group = dims.num_q_heads / dims.num_kv_heads;
+  const int32_t waves = extend_waves(dims.head_dim, group);
+  const int32_t tb = waves * 32 / group;  // tokens per item: waves*32 rows of (token, head)
+  const int32_t hkv = dims.num_kv_heads;
+  plan->waves = waves;
+  plan->tokens_per_item = tb;
+  // one workgroup-tile: 64 keys against 256 query rows, two products
+  const double tile_us = 4.0 * kExtendKeyTile * (waves * 32) * dims.head_dim / kCuFlopsPerUs;
+
+  // Blocks of each task, latest first (later blocks see more keys).
+  const int32_t ntasks = (int32_t)tasks.size();
+  std::vector<int32_t> task_first((size_t)ntasks + 1, 0);
+  int64_t nblocks = 0;
+  for (int32_t b = 0; b < ntasks; ++b) nblocks += (tasks[b].extend + tb - 1) / tb;
+  if (nblocks * hkv > INT32_MAX / 4) return TIDE_ERR_INVALID_ARG;
+  std::vector<Block> blocks;
+  blocks.reserve((size_t)nblocks);
+  for (int32_t b = 0; b < ntasks; ++b) {
+    task_first[b] = (int32_t)blocks.size();
+    const int32_t p = tasks[b].prefix, e = tasks[b].extend;
+    for (int32_t k = (e + tb - 1) / tb - 1; k >= 0; --k) {
+      Block bl;
+      bl.task = b;
+      bl.tok0 = k * tb;
+      bl.ntok = std::min(tb, e - k * tb);
+      bl.ntiles = (int32_t)(((int64_t)p + bl.tok0 + bl.ntok + kExtendKeyTile - 1) / kExtendKeyTile);
+      blocks.push_back(bl);
+    }
+  }
+  task_first[ntasks] = (int32_t)blocks.size();
+  const int64_t plain_items = nblocks * hkv;
+
+  // TIDE_EXTEND_SPLIT=0 keeps the plain plan, =1 takes the best split plan whenever one
+  // exists (both for tests and tuning); otherwise the estimate decides.
+  const char* env = getenv("TIDE_EXTEND_SPLIT");
+  const int mode = (env && env[0] == '0') ? 0 : (env && env[0] == '1') ? 1 : -1;
+  int32_t T = 0;
+  if (mode != 0 && plain_items > 0 && plain_items <= kSplitMaxItems) {
+    int64_t slots = 0;
+    const double plain_us =
+        estimate(blocks, hkv, dims.num_q_heads, dims.head_dim, 0, tile_us, &slots);
+    plan->est_plain_us = plan->est_us = plain_us;
+    double best_us = mode == 1 ? INFINITY : plain_us * kSplitGain;
+    int64_t tiles = 0;
+    for (const Block& b : blocks) tiles += b.ntiles;
+    int64_t last = -1;
+    for (int rounds = 1; rounds <= 4; ++rounds) {
+      const int64_t t = std::max<int64_t>(
+          kMinChunkTiles, (tiles * hkv + (int64_t)rounds * kCus - 1) / ((int64_t)rounds * kCus));
+      if (t > INT32_MAX / 2 || t == last) continue;
+      last = t;
+      const double us =
+          estimate(blocks, hkv, dims.num_q_heads, dims.head_dim, (int32_t)t, tile_us, &slots);
+      if (slots > 0 && slots <= INT32_MAX / 2 && us < best_us) {
+        best_us = plan->est_us = us;
+        T = (int32_t)t;
+      }
+    }
+  }
+
+  std::vector<int32_t> nchunks(blocks.size());
+  for (size_t k = 0; k < blocks.size(); ++k) nchunks[k] = num_chunks(blocks[k].ntiles, T);
+  const std::vector<std::vector<Piece>> queues = place(blocks, task_first, nchunks, hkv, T);
+  plan->split = T > 0;
+  if (T == 0) {
+    const std::vector<ExtendItem> items = interleave<ExtendItem>(
+        queues, [&](int32_t k, int32_t g, int32_t) {
+          return ExtendItem{blocks[k].task, g, blocks[k].tok0, blocks[k].ntok};
+        });
+    *n_items = (int64_t)items.size();
+    if (build_blob) to_bytes(items, items_bytes);
+    return TIDE_OK;
+  }
+
+  // partial row slots of the split blocks
+  std::vector<int32_t> pbase(blocks.size(), 0);
+  int64_t slots = 0;
+  for (size_t k = 0; k < blocks.size(); ++k)
+    if (nchunks[k] > 1) {
+      pbase[k] = (int32_t)slots;
+      slots += (int64_t)blocks[k].ntok * nchunks[k];
+    }
+  plan->row_slots = slots;
+  const std::vector<ExtendChunkItem> items = interleave<ExtendChunkItem>(
+      queues, [&](int32_t k, int32_t g, int32_t c) {
+        const int32_t n = nchunks[k];
+        ExtendChunkItem it;
+        it.task = blocks[k].task;
+        it.kv_head = g;
+        it.tok0 = blocks[k].tok0;
+        it.ntok = blocks[k].ntok;
+        it.t_begin = c * T;
+        it.t_end = it.t_begin + chunk_tiles(blocks[k].ntiles, T, n, c);
+        it.split = n > 1 ? c : -1;
+        it.pbase = pbase[k];
+        return it;
+      });
+  *n_items = (int64_t)items.size();
+  if (build_blob) {
+    to_bytes(items, items_bytes);
+    std::vector<MergeRow> rows((size_t)plan->total_rows, MergeRow{0, 0, 0, 0});
+    for (size_t k = 0; k < blocks.size(); ++k) {
+      if (nchunks[k] < 2) continue;
+      const int32_t r0 = tasks[blocks[k].task].row_start + blocks[k].tok0;
+      for (int32_t tk = 0; tk < blocks[k].ntok; ++tk)
+        rows[r0 + tk] = MergeRow{pbase[k] + tk, blocks[k].ntok, nchunks[k], 0};
+    }
+    to_bytes(rows, merge_bytes);
+  }
+  return TIDE_OK;
+}
+
+}  // namespace
+
 int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* lens_b,
               const tide_dims& dims, int32_t num_splits, int32_t bt_stride, bool build_blob,
               Plan* plan) {
@@ -76,7 +361,6 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
   int rc = check_dims(&dims);
   if (rc != TIDE_OK) return rc;
 
-  const int32_t group = dims.num_q_heads / dims.num_kv_heads;
   *plan = Plan();
   plan->op = op;
   plan->num_tasks = num_tasks;
@@ -100,7 +384,7 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
   plan->total_rows = (int32_t)rows;
 
   // ---- work items -------------------------------------------------------------------
-  std::vector<uint8_t> items_bytes;
+  std::vector<uint8_t> items_bytes, merge_bytes;
   int64_t n_items = 0;
   if (op == TIDE_OP_KV_APPEND) {
     std::vector<AppendItem> items;
@@ -122,65 +406,8 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
       if (!items.empty()) memcpy(items_bytes.data(), items.data(), items_bytes.size());
     }
   } else if (op == TIDE_OP_EXTEND || op == TIDE_OP_FULL_PREFILL) {
-    const int32_t waves = extend_waves(dims.head_dim, group);
-    const int32_t tb = waves * 32 / group;  // tokens per item: waves*32 rows of (token, head)
-    plan->waves = waves;
-    plan->tokens_per_item = tb;
-    // Work units are (task, kv head): all query blocks of a unit read the same K/V.
-    // Workgroups are dispatched round-robin over the XCDs (item i runs on XCD i % 8),
-    // each with its own L2.  Every unit is placed on one XCD, its blocks consecutive in
-    // that XCD's order, so the blocks that walk the same K/V run side by side and share
-    // it through L2 instead of re-reading HBM.  Units go longest first to the least
-    // loaded XCD; inside a unit the longest blocks go first.
-    struct Unit {
-      int64_t cost;
-      int32_t task, kv_head;
-    };
-    std::vector<Unit> units;
-    for (int32_t b = 0; b < num_tasks; ++b) {
-      const int32_t p = tasks[b].prefix, e = tasks[b].extend;
-      if (e == 0) continue;
-      int64_t cost = 0;
-      for (int32_t t0 = 0; t0 < e; t0 += tb) {
-        const int32_t n = std::min(tb, e - t0);
-        cost += (int64_t)n * ((int64_t)p + t0 + n);
-      }
-      for (int32_t g = 0; g < dims.num_kv_heads; ++g) units.push_back({cost, b, g});
-    }
-    std::stable_sort(units.begin(), units.end(),
-                     [](const Unit& x, const Unit& y) { return x.cost > y.cost; });
-    std::vector<std::vector<ExtendItem>> queues(kXcds);
-    std::vector<int64_t> load(kXcds, 0);
-    for (const Unit& u : units) {
-      const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-      load[x] += u.cost;
-      const int32_t p = tasks[u.task].prefix, e = tasks[u.task].extend;
-      const int32_t nblk = (e + tb - 1) / tb;
-      for (int32_t k = nblk - 1; k >= 0; --k) {  // later blocks see more keys
-        ExtendItem it;
-        it.task = u.task;
-        it.kv_head = u.kv_head;
-        it.tok0 = k * tb;
-        it.ntok = std::min(tb, e - k * tb);
-        queues[x].push_back(it);
-      }
-      (void)p;
-    }
-    size_t depth = 0;
-    for (const auto& qx : queues) depth = std::max(depth, qx.size());
-    std::vector<ExtendItem> items(depth * kXcds);
-    for (size_t i = 0; i < depth; ++i)
-      for (int x = 0; x < kXcds; ++x) {
-        ExtendItem it = {0, 0, 0, 0};  // ntok == 0: an empty slot the kernel skips
-        if (i < queues[x].size()) it = queues[x][i];
-        items[i * kXcds + x] = it;
-      }
-    while (!items.empty() && items.back().ntok == 0) items.pop_back();
-    n_items = (int64_t)items.size();
-    if (build_blob) {
-      items_bytes.resize(items.size() * sizeof(ExtendItem));
-      if (!items.empty()) memcpy(items_bytes.data(), items.data(), items_bytes.size());
-    }
+    rc = plan_extend(tasks, dims, build_blob, plan, &items_bytes, &merge_bytes, &n_items);
+    if (rc != TIDE_OK) return rc;
   } else {  // decode
     int64_t chunk = 0;
     if (num_splits > 0) {
@@ -222,14 +449,26 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
   }
   if (n_items > INT32_MAX / 4) return TIDE_ERR_INVALID_ARG;
   plan->num_items = (int32_t)n_items;
+  const size_t item_size = plan->split ? sizeof(ExtendChunkItem) : 16;
 
   // ---- layout -------------------------------------------------------------------------
   size_t off = sizeof(WsHeader);
   plan->tasks_off = off;
   off = align_up(off + tasks.size() * sizeof(TaskDesc), kWsAlign);
   plan->items_off = off;
-  off = align_up(off + (size_t)n_items * 16, kWsAlign);
+  off = align_up(off + (size_t)n_items * item_size, kWsAlign);
+  if (plan->split) {
+    plan->merge_rows_off = off;
+    off = align_up(off + (size_t)plan->total_rows * sizeof(MergeRow), kWsAlign);
+  }
   plan->upload_bytes = off;
+  if (plan->split) {
+    const size_t slots = (size_t)plan->row_slots * dims.num_q_heads;
+    plan->part_o_off = off;
+    off = align_up(off + slots * dims.head_dim * sizeof(float), kWsAlign);
+    plan->part_ml_off = off;
+    off = align_up(off + slots * 4 * sizeof(float), kWsAlign);
+  }
   if (op == TIDE_OP_DECODE) {
     const size_t slots = (size_t)num_tasks * dims.num_q_heads * (size_t)plan->max_splits;
     plan->part_o_off = off;
@@ -245,6 +484,8 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
       memcpy(plan->blob.data() + plan->tasks_off, tasks.data(), tasks.size() * sizeof(TaskDesc));
     if (!items_bytes.empty())
       memcpy(plan->blob.data() + plan->items_off, items_bytes.data(), items_bytes.size());
+    if (plan->split && !merge_bytes.empty())
+      memcpy(plan->blob.data() + plan->merge_rows_off, merge_bytes.data(), merge_bytes.size());
   }
   return TIDE_OK;
 }

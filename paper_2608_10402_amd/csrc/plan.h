@@ -21,7 +21,15 @@ struct Plan {
   size_t tasks_off = 0;
   size_t items_off = 0;
   size_t upload_bytes = 0;
-  // decode partials (not uploaded)
+  // extend split-KV plan: per-row merge descriptors (uploaded after the items)
+  bool split = false;
+  size_t merge_rows_off = 0;
+  int64_t row_slots = 0;  // partial row slots (each holds every query head)
+  // the planner's run-time estimates (microseconds) of the plain and chosen extend plans;
+  // 0 when the call was too large to consider splitting
+  double est_plain_us = 0.0;
+  double est_us = 0.0;
+  // decode and split-extend partials (not uploaded)
   size_t part_o_off = 0;
   size_t part_ml_off = 0;
   size_t total_bytes = 0;

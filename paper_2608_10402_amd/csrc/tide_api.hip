@@ -152,10 +152,15 @@ int run_extend(int op, const void* q, const void* k_pool, const void* v_pool, in
   a.scale_log2 = dims->sm_scale * 1.44269504088896340736f;
   a.num_items = plan.num_items;
   a.tasks = at<TaskDesc>(workspace, plan.tasks_off);
-  a.items = at<ExtendItem>(workspace, plan.items_off);
+  a.items = plan.split ? nullptr : at<ExtendItem>(workspace, plan.items_off);
   a.out = static_cast<uint16_t*>(out);
   a.lse = lse;
   a.error_flags = at_mut<int32_t>(workspace, 0);
+  a.chunk_items = plan.split ? at<ExtendChunkItem>(workspace, plan.items_off) : nullptr;
+  a.merge_rows = plan.split ? at<MergeRow>(workspace, plan.merge_rows_off) : nullptr;
+  a.part_o = plan.split ? at_mut<float>(workspace, plan.part_o_off) : nullptr;
+  a.part_ml = plan.split ? at_mut<float>(workspace, plan.part_ml_off) : nullptr;
+  a.total_rows = plan.total_rows;
   return finish(launch_extend(a, dims->head_dim, plan.waves, s), workspace, s);
 }
 

@@ -32,6 +32,33 @@ struct ExtendItem {
   int32_t ntok;
 };
 
+// Extend / prefill work item of the split-KV plan, used when a call has too few items
+// to fill the chip: key tiles [t_begin, t_end) of the item (64 keys each, counted from
+// key 0).  split >= 0: one of the item's chunks; its unnormalised partial for row slot
+// s = pbase + split * ntok + tk (tk = token inside the item) and query head h goes to
+// part_o[(s * Hq + h) * d] and part_ml[(s * Hq + h) * 4], and a merge combines the
+// chunks.  split == -1: the item is not split and writes its output directly.
+struct ExtendChunkItem {
+  int32_t task;
+  int32_t kv_head;
+  int32_t tok0;
+  int32_t ntok;
+  int32_t t_begin;
+  int32_t t_end;
+  int32_t split;
+  int32_t pbase;
+};
+
+// Merge descriptor of one packed extend row: its partials sit in row slots base,
+// base + stride, ..., base + (nsplit - 1) * stride; nsplit == 0 means the row was
+// written directly and has nothing to merge.
+struct MergeRow {
+  int32_t base;
+  int32_t stride;
+  int32_t nsplit;
+  int32_t pad;
+};
+
 // Decode split-K item: keys [k_begin, min(kv_len, k_begin + chunk)) of one (task, kv head).
 struct DecodeItem {
   int32_t task;
@@ -101,6 +128,14 @@ struct ExtendArgs {
   uint16_t* out;
   float* lse;
   int32_t* error_flags;
+  // split-KV plan (chunk_items non-null): items, per-row merge descriptors and the
+  // partial buffers [row slots][Hq][d] and [row slots][Hq][4] (max in base-2 units, sum of
+  // the bf16-rounded weights, exact fp32 sum, unused)
+  const ExtendChunkItem* chunk_items;
+  const MergeRow* merge_rows;
+  float* part_o;
+  float* part_ml;
+  int32_t total_rows;
 };
 
 struct DecodeArgs {

@@ -60,6 +60,71 @@ __device__ __forceinline__ float xor_shfl(float v, int mask) {
   return __shfl_xor(v, mask, 64);
 }
 
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, xor_shfl(v, m));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += xor_shfl(v, m);
+  return v;
+}
+
+// One wave combines n >= 1 split partials of one (row, query head), the split-K merge of
+// flash decoding: partial s holds, at ml + s * ml_stride, its running max m_s (base-2
+// units), the sum of its bf16-rounded weights and their exact fp32 sum, and at
+// po + s * po_stride its unnormalised output.  With M = max m_s and w_s = 2^(m_s - M) the
+// row is sum_s w_s o_s / sum_s w_s l_s, written as bf16 to orow; when lse_out is non-null
+// it receives ln(sum_s w_s l_exact_s) + M ln 2.  Lane s owns split s for the statistics;
+// the outputs are accumulated with every lane covering D/64 entries.
+template <int D>
+__device__ __forceinline__ void merge_partials(const float* ml, int64_t ml_stride, const float* po,
+                                               int64_t po_stride, int n, uint16_t* orow,
+                                               float* lse_out) {
+  const int lane = threadIdx.x & 63;
+  constexpr int kPer = D / 64;
+  float mx = kNoMax;
+  for (int s = lane; s < n; s += 64) mx = fmaxf(mx, ml[s * ml_stride]);
+  mx = wave_max(mx);
+
+  float acc[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) acc[i] = 0.0f;
+  float l_round = 0.0f, l_ex = 0.0f;
+  for (int s0 = 0; s0 < n; s0 += 64) {
+    const int s = s0 + lane;
+    float wgt = 0.0f;
+    if (s < n) {
+      const f32x4 st = *reinterpret_cast<const f32x4*>(ml + s * ml_stride);
+      wgt = fast_exp2(st[0] - mx);
+      l_round += wgt * st[1];
+      l_ex += wgt * st[2];
+    }
+    const int cnt = min(64, n - s0);
+#pragma unroll 4
+    for (int i = 0; i < cnt; ++i) {
+      const float wi = __shfl(wgt, i, 64);
+      const float* src = po + (int64_t)(s0 + i) * po_stride + kPer * lane;
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) acc[k] += wi * src[k];
+    }
+  }
+  l_round = wave_sum(l_round);
+  const float inv = 1.0f / l_round;
+  if (kPer == 2) {
+    *reinterpret_cast<uint32_t*>(orow + 2 * lane) = pack_bf16x2(acc[0] * inv, acc[kPer - 1] * inv);
+  } else {
+    const uint32_t w = pack_bf16x2(acc[0] * inv, 0.0f);
+    orow[lane] = (uint16_t)(w & 0xFFFFu);
+  }
+  if (lse_out) {
+    l_ex = wave_sum(l_ex);
+    if (lane == 0) *lse_out = (mx + __log2f(l_ex)) * kLn2;
+  }
+}
+
 // v_mfma_f32_32x32x16_bf16.  Lane layouts (checked on gfx950):
 //   A: lane l holds row l%32, k = 8*(l/32) .. +7;  B: lane l holds column l%32, same k;
 //   D: lane l register r holds row 8*(r/4) + 4*(l/32) + r%4, column l%32.

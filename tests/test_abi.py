@@ -96,11 +96,18 @@ def test_length_validation():
     assert _ws(99, [1], [1], GOOD)[0] == tide.TIDE_ERR_INVALID_ARG
 
 
-def test_workspace_sizes_are_consistent():
+def test_workspace_sizes_are_consistent(monkeypatch):
+    monkeypatch.setenv("TIDE_EXTEND_SPLIT", "0")  # the plain plan: no partials
     rc, a = _ws(tide.TIDE_OP_EXTEND, [100, 2000], [10, 300], GOOD)
     assert rc == 0 and a > 0
     rc, b = _ws(tide.TIDE_OP_EXTEND, [100, 2000], [10, 3000], GOOD)
     assert rc == 0 and b >= a  # more rows, more work items
+    monkeypatch.setenv("TIDE_EXTEND_SPLIT", "1")  # the split plan adds fp32 partials
+    rc, a1 = _ws(tide.TIDE_OP_EXTEND, [100, 2000], [10, 300], GOOD)
+    assert rc == 0 and a1 > a
+    monkeypatch.delenv("TIDE_EXTEND_SPLIT")
+    rc, a2 = _ws(tide.TIDE_OP_EXTEND, [100, 2000], [10, 300], GOOD)
+    assert rc == 0 and a2 in (a, a1)
     rc, p = _ws(tide.TIDE_OP_FULL_PREFILL, [110, 2300], None, GOOD)
     assert rc == 0 and p > 0
     rc, d1 = _ws(tide.TIDE_OP_DECODE, [5000, 9000], None, GOOD, splits=1)
