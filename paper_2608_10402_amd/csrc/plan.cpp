@@ -548,9 +548,13 @@ int make_plan_shared(int32_t num_tasks, const int32_t* kv_lens, int32_t num_grou
   for (int32_t g = 0; g < (num_tasks > 0 ? num_groups : 0); ++g) {
     const int32_t s0 = group_start[g], s1 = group_start[g + 1], sh = shared_lens[g];
     const int32_t np = (int32_t)ceil_div(sh, chunk);
-    for (int32_t f = s0; f < s1; f += per_item)
-      for (int32_t h = 0; h < dims.num_kv_heads; ++h)
-        for (int32_t j = 0; j < np; ++j) {
+    // The items of one (kv head, chunk) -- one per run of per_item trajectories -- read the
+    // same prefix keys.  They are consecutive, so they share a workgroup of the decode
+    // kernel (four waves, one item each, on one CU) or a neighbouring one, and the later
+    // reads hit that XCD's L2.
+    for (int32_t h = 0; h < dims.num_kv_heads; ++h)
+      for (int32_t j = 0; j < np; ++j)
+        for (int32_t f = s0; f < s1; f += per_item) {
           SharedDecodeItem it = {};
           it.first_task = f;
           it.ntasks = std::min(per_item, s1 - f);
