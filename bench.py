@@ -526,6 +526,9 @@ def main():
                                      "unit": "GB/s", "frac": round(vp / PEAK_HBM_GBS, 4)}
         extra.update({
             "speedup_shared_vs_plain_decode": round(t_p / t_s, 3),
+            # plain decode streams every page with the non-temporal hint, so the group's
+            # shared prompt pages are re-read from HBM rather than L2
+            "plain_decode_cache_policy": "non-temporal",
             "shared_decode_plain_equivalent_GBps": round(st_p.bytes / (t_s * 1e-3) / 1e9, 1),
             "decode_tokens_per_s": round(wl.num_tasks / (t_s * 1e-3), 1),
             "shared_vs_plain_max_abs_diff": float((keep["out_shared"].float() -

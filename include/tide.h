@@ -171,6 +171,10 @@ TIDE_API int tide_extend_attn(const void* q, const void* k_pool, const void* v_p
  * parallel and merged by log-sum-exp weights (split-K).  num_splits == 0 chooses the
  * chunk size automatically; num_splits > 0 caps the number of chunks per task at that
  * value.  Results for different split counts agree to fp32 rounding.
+ * Every K/V page is streamed with the non-temporal cache hint, since each task's context
+ * is read once.  Tasks whose block tables share pages (a GRPO group's prompt) should go
+ * through tide_decode_attn_shared, which reads a shared prefix once per group; here each
+ * task re-reads it from HBM.
  */
 TIDE_API int tide_decode_attn(const void* q, const void* k_pool, const void* v_pool, int64_t num_pages,
                      const int32_t* block_table, int32_t bt_stride, int32_t num_tasks,
