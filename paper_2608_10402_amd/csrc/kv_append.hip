@@ -5,10 +5,10 @@
 // so that attention reads V^T operands with plain 16-byte loads.
 //
 // One wave per (task, logical page, kv head).  K rows are copied with 16-byte loads and
-// stores.  V rows are staged in LDS and written back transposed as 2-byte stores in
-// which consecutive lanes cover consecutive slots of one head-dim row, so each store
-// instruction writes whole 32-byte rows of the page for full pages.  Only slots of the
-// positions being appended are written: a partially filled page keeps its other slots.
+// stores.  V rows are staged in LDS and written back transposed: a page filled by this
+// append takes 16-byte stores (half a head-dim row of 8 slots each); a page that is only
+// partly appended takes 2-byte stores of exactly its new slots, consecutive lanes
+// covering consecutive slots of one head-dim row, so it keeps its other slots.
 #include "kernels.h"
 #include "tide_device.h"
 
@@ -36,7 +36,27 @@ __global__ __launch_bounds__(kWaves * 64) void kv_append_kernel(AppendArgs a) {
   const int64_t blk = ((int64_t)(active ? phys : 0) * a.num_kv_heads + g) * (int64_t)(kPage * D);
   uint16_t* vl = v_lds[wave];
 
-  if (active) {
+  if (active && n == kPage) {
+    // Full page: every lane issues all its loads (kPage * D / 8 / 64 K and V pieces)
+    // before any store, so they are in flight together.
+    constexpr int kPer = kPage * (D / 8) / 64;
+    u32x4 kk[kPer], vv[kPer];
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int idx = lane + 64 * i, sl = idx / (D / 8), part = idx % (D / 8);
+      const int64_t src = ((row0 + sl) * a.num_kv_heads + g) * D + part * 8;
+      kk[i] = load_u32x4(a.k_new + src);
+      vv[i] = load_u32x4(a.v_new + src);
+    }
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int idx = lane + 64 * i, sl = idx / (D / 8), part = idx % (D / 8);
+      store_u32x4(a.k_pool + blk + sl * D + part * 8, kk[i]);
+      uint32_t* dst = reinterpret_cast<uint32_t*>(vl + sl * kPitch + part * 8);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) dst[w] = vv[i][w];
+    }
+  } else if (active) {
     for (int idx = lane; idx < n * (D / 8); idx += 64) {
       const int sl = idx / (D / 8), part = idx % (D / 8);
       const int64_t src = ((row0 + sl) * a.num_kv_heads + g) * D + part * 8;
@@ -48,7 +68,18 @@ __global__ __launch_bounds__(kWaves * 64) void kv_append_kernel(AppendArgs a) {
     }
   }
   __syncthreads();
-  if (active) {
+  if (active && n == kPage) {
+    // Full page: each V^T row (16 slots, 32 bytes) is two 16-byte stores, one per half.
+    for (int idx = lane; idx < D * 2; idx += 64) {
+      const int d = idx >> 1, h = idx & 1;
+      u32x4 w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        w[e] = (uint32_t)vl[(8 * h + 2 * e) * kPitch + d] |
+               ((uint32_t)vl[(8 * h + 2 * e + 1) * kPitch + d] << 16);
+      store_u32x4(a.v_pool + blk + d * kPage + 8 * h, w);
+    }
+  } else if (active) {
     for (int idx = lane; idx < D * kPage; idx += 64) {
       const int d = idx / kPage, s = idx % kPage;
       if (s >= s0 && s < s0 + n) a.v_pool[blk + d * kPage + s] = vl[s * kPitch + d];
