@@ -39,7 +39,10 @@ TFLOP/s over the unmasked (query, key) pairs (4*d flops per pair and query head)
 resumed_decode it is decode-attention GB/s of algorithmic bytes, and for grpo_group_decode
 the shared-prefix decode's GB/s over the bytes it must read (each prompt once per group).  The line also carries
 the other stages' rates, the speedup of extend over re-prefill, the roofline of the
-dominant kernel, and the fp64 oracle timed on a bounded sample on the host.
+dominant kernel, and the fp64 oracle timed on a bounded sample on the host.  For extend
+workloads, `extra.one_task_resume` times a resume round of a single task (the longest
+prefix) outside the step, under the plain plan and under the planner's choice, which
+splits the keys of a call that has too few work items for the chip.
 """
 from __future__ import annotations
 
@@ -261,6 +264,47 @@ def build_stages(wl, kv, dev, args, torch, np_up):
                                 (lambda qn=qn, on=on, pos=pos: kv.decode(qn, pos + 1, out=on)),
                                 bytes_=decode_bytes(wl, pos + 1)))
     return stages, keep
+
+
+def one_task_resume(wl, kv, keep, steps, torch, stream):
+    """A resume round that holds a single task: the workload's longest-prefix task alone,
+    timed under the plain plan and under the planner's own choice (which is split-KV when
+    one task leaves most compute units idle).  Outside the timed step."""
+    s = wl.spec
+    b = int(np.argmax(wl.prefix_lens))
+    indptr = np.concatenate([[0], np.cumsum(wl.extend_lens)]).astype(np.int64)
+    q = keep["q_ext"][int(indptr[b]):int(indptr[b + 1])]
+    out = torch.empty_like(q)
+    ext = np.zeros(wl.num_tasks, np.int32)
+    ext[b] = wl.extend_lens[b]
+    p, e = float(wl.prefix_lens[b]), float(wl.extend_lens[b])
+    flops = 4.0 * s.head_dim * s.num_q_heads * (e * p + e * (e + 1) / 2)
+    res = {"task": b, "prefix": int(p), "extend": int(e)}
+    saved = os.environ.get("TIDE_EXTEND_SPLIT")
+    try:
+        for name, mode in (("plain", "0"), ("auto", None)):
+            if mode is None:
+                os.environ.pop("TIDE_EXTEND_SPLIT", None)
+            else:
+                os.environ["TIDE_EXTEND_SPLIT"] = mode
+            for _ in range(3):
+                kv.extend(q, wl.prefix_lens, ext, out=out)
+            ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            ea.record(stream)
+            for _ in range(steps):
+                kv.extend(q, wl.prefix_lens, ext, out=out)
+            eb.record(stream)
+            torch.cuda.synchronize()
+            t = ea.elapsed_time(eb) / steps
+            res[name + "_ms"] = round(t, 4)
+            res[name + "_TFLOPs"] = round(flops / (t * 1e-3) / 1e12, 1)
+    finally:
+        if saved is None:
+            os.environ.pop("TIDE_EXTEND_SPLIT", None)
+        else:
+            os.environ["TIDE_EXTEND_SPLIT"] = saved
+    res["speedup_auto_vs_plain"] = round(res["plain_ms"] / res["auto_ms"], 3)
+    return res
 
 
 CTB_POOL_PAGES = 57344   # 917,504 tokens: a 7B model's KV budget on an 80 GB GPU
@@ -489,6 +533,7 @@ def main():
         rooflines["extend"] = {"bound": "mfma", "achieved": round(v, 2), "peak": PEAK_BF16_TFLOPS,
                                "unit": "TFLOP/s", "frac": round(v / PEAK_BF16_TFLOPS, 4)}
         extra["extend_tokens_per_s"] = round(float(wl.extend_lens.sum()) / (t * 1e-3), 1)
+        extra["one_task_resume"] = one_task_resume(wl, kv, keep, args.steps, torch, stream)
     if "prefill" in ms:
         t, f, _ = total("prefill")
         v = f / (t * 1e-3) / 1e12

@@ -73,9 +73,9 @@ int task_lengths(int op, int32_t b, const int32_t* lens_a, const int32_t* lens_b
 //          merges (the split-K scheme of flash decoding, applied to extend blocks).
 // Splitting pays when a call has too few items to keep 256 CUs busy to the end.  The
 // choice compares closed-form run-time estimates: the makespan of n workgroups costing
-// c_i tiles each on 256 CUs is taken as max(max c, sum c / 256 + max c / 2), a tile costs
-// less while few CUs are busy (the clock is higher), and a split plan adds the merge's
-// HBM traffic and launch.  The planner runs on every call, so everything here is linear
+// c_i tiles each on 256 CUs is max c when n <= 256 (all start at once), and is taken as
+// max(max c, sum c / 256 + max c / 2) otherwise; a tile costs less while few CUs are
+// busy (the clock is higher), and a split plan adds the merge's HBM traffic and launch.  The planner runs on every call, so everything here is linear
 // in the number of blocks, and only the chosen plan is materialised.
 namespace {
 
@@ -129,7 +129,9 @@ double estimate(const std::vector<Block>& blocks, int32_t num_kv_heads, int32_t 
   total *= num_kv_heads;
   const double busy = std::min(1.0, (double)items / kCus);
   const double t_eff = tile_us * (1.0 - kIdleClockGain * (1.0 - busy));
-  double us = std::max(biggest, total / kCus + 0.5 * biggest) * t_eff;
+  // up to one workgroup per CU, all start at once and the longest one ends the call
+  const double span = items <= kCus ? biggest : std::max(biggest, total / kCus + 0.5 * biggest);
+  double us = span * t_eff;
   if (slots > 0)
     us += (double)slots * num_q_heads * (head_dim * 4.0 + 16.0) * 2.0 / kHbmBytesPerUs +
           kMergeLaunchUs;
