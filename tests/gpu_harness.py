@@ -124,7 +124,7 @@ def oracle_task_rows(wl: W.Workload, b: int, rows, upto: int | None = None,
     """fp64 oracle for selected query positions of task b, from a compact pool that holds
     only task b (its own append, its own page order).  `rows` are absolute positions;
     each attends to keys 0..row.  `upto` = number of positions to place (default: the
-    last requested row + 1).  Returns (out [n, Hq, d], lse [n, Hq])."""
+    last requested row + 1).  Returns (sorted rows, out [n, Hq, d], lse [n, Hq])."""
     s = wl.spec
     rows = np.asarray(sorted(rows), dtype=np.int64)
     n_pos = int(upto if upto is not None else rows.max() + 1)

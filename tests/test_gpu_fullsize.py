@@ -8,6 +8,7 @@ full fragmented pool.  Physical placement does not change the result (pinned for
 oracle on the CPU), so the comparison is exact up to the GPU's bf16 rounding.
 """
 import gc
+import os
 
 import numpy as np
 import pytest
@@ -78,6 +79,38 @@ def test_agent_resume_extend(agent_resume):
     out, lse = dw.extend()
     _check_extend_rows(wl, out, lse, sample_tasks(wl, 4, seed=1))
     _check_append_pages(wl, dw, sample_tasks(wl, 2, seed=2), lambda b: int(wl.seq_lens[b]))
+
+
+def test_agent_resume_one_task_split(agent_resume):
+    """The bench's one-task resume: the longest-prefix task alone, which the planner runs
+    split-KV (a few dozen items for 256 CUs).  Sampled rows against the oracle, and the
+    split rows against the same task's rows from the plain plan."""
+    wl, dw = agent_resume
+    b = int(np.argmax(wl.prefix_lens))
+    indptr = np.concatenate([[0], np.cumsum(wl.extend_lens)]).astype(np.int64)
+    q = dev_bf16(wl.packed("q", wl.extend_ranges()))[int(indptr[b]):int(indptr[b + 1])]
+    ext = np.zeros(wl.num_tasks, np.int32)
+    ext[b] = wl.extend_lens[b]
+    outs = {}
+    for mode in ("1", "0"):
+        os.environ["TIDE_EXTEND_SPLIT"] = mode
+        try:
+            lse = torch.empty((q.shape[0], q.shape[1]), dtype=torch.float32, device=q.device)
+            outs[mode] = (dw.kv.extend(q, wl.prefix_lens, ext, lse=lse), lse)
+        finally:
+            os.environ.pop("TIDE_EXTEND_SPLIT", None)
+    torch.cuda.synchronize()
+    p, e = int(wl.prefix_lens[b]), int(wl.extend_lens[b])
+    rng = np.random.default_rng(5)
+    local = sorted(set([0, e - 1] + rng.integers(0, e, size=6).tolist()))
+    pos, o, l = oracle_task_rows(wl, b, [p + j for j in local], upto=p + e)
+    rows = torch.as_tensor(local, device=q.device)
+    out_s, lse_s = outs["1"]
+    assert_close(out_s[rows], o, "agent_resume_7b one-task split sampled")
+    assert_lse(lse_s[rows], l, "agent_resume_7b one-task split sampled")
+    d = (out_s.float() - outs["0"][0].float()).abs()
+    log("one-task split vs plain: max %.3g mean %.3g" % (d.max().item(), d.mean().item()))
+    assert d.max().item() <= 2e-2 and d.mean().item() <= 2e-3
 
 
 def test_agent_resume_prefill_and_equivalence(agent_resume):
