@@ -158,9 +158,11 @@ class Replay:
     rows(which, tasks, p0, p1) must return rows p0[i]..p1[i]-1 of every task tasks[i],
     concatenated: [sum n, heads, d] with heads the query heads for "q" and the KV heads
     for "k" / "v" -- either as a bf16 device tensor, or as bf16 bit patterns (uint16
-    numpy) that are uploaded.  Each round's inputs are ready before its kernels are
-    queued, so per-stage events bracket only the library calls (their work-list uploads
-    and kernels).
+    numpy) that are uploaded.  A source whose rows live on the device may also offer
+    locate(tasks, p0, p1) -> locator and fetch(which, locator) -> tensor, so that a
+    round can be prepared (locators, block tables) before it is executed.  Each round's
+    inputs are ready before its kernels are queued, so per-stage events bracket only the
+    library calls (their work-list uploads and kernels).
     """
 
     def __init__(self, kv: PagedKV, rows, rank: int = 0, with_lse: bool = False):
@@ -182,45 +184,71 @@ class Replay:
             bt[j, : n[j]] = rnd.op_pages(i)
         return bt
 
+    def _to_device(self, arr: np.ndarray) -> torch.Tensor:
+        """Host array -> device through a pinned copy, so that the host does not wait for
+        the GPU to drain (a copy from pageable memory synchronises the stream): the host
+        queues the next rounds while the GPU runs, and the events time GPU work only."""
+        t = torch.from_numpy(np.ascontiguousarray(arr))
+        if self.kv.device.type != "cuda":
+            return t.to(self.kv.device)
+        return t.pin_memory().to(self.kv.device, non_blocking=True)
+
     def _up(self, rows) -> torch.Tensor:
         if isinstance(rows, torch.Tensor):
             return rows
-        t = torch.from_numpy(np.ascontiguousarray(rows).view(np.int16))
-        return t.to(self.kv.device).view(torch.bfloat16)
+        return self._to_device(np.ascontiguousarray(rows).view(np.int16)).view(torch.bfloat16)
 
-    def run(self, rnd: Round, timed: bool = True) -> dict:
-        """Executes the round's ops of this rank.  Returns the device outputs:
-        {"extend": (op indices, out, lse), "decode": (op indices, out, lse)}."""
-        kv, dev = self.kv, self.kv.device
-        d = self.kv.dims
+    def prepare(self, rnd: Round) -> list:
+        """Everything a round needs on the device, taken from the scheduler's round while
+        it is valid: per op kind the op indices, lengths, block table (on the device), the
+        rows to attend (a device-side locator when the row source offers one, see
+        `execute`) and the workspace size.  Preparing every round first and executing them
+        afterwards keeps host work out of the timed calls."""
         ops = rnd.ops
+        d = self.kv.dims
         mine = np.nonzero(ops["rank"] == self.rank)[0]
-        result = {}
+        prepared = []
         for kind, name in ((OP_EXTEND, "extend"), (OP_DECODE, "decode")):
             idx = mine[ops["kind"][mine] == kind]
             if idx.size == 0:
                 continue
-            tasks = ops["task"][idx]
+            tasks = ops["task"][idx].copy()
             start = ops["start"][idx].astype(np.int32)
             count = ops["count"][idx].astype(np.int32)
-            bt = torch.from_numpy(self._table(rnd, idx)).to(dev)
-            k = self._up(self.rows("k", tasks, start, start + count))
-            v = self._up(self.rows("v", tasks, start, start + count))
-            q = self._up(self.rows("q", tasks, start, start + count))
+            if kind == OP_EXTEND:
+                ws = max(_lib.tide_workspace_size(_lib.TIDE_OP_KV_APPEND, start, count, d),
+                         _lib.tide_workspace_size(_lib.TIDE_OP_EXTEND, start, count, d))
+            else:
+                ws = _lib.tide_workspace_size(_lib.TIDE_OP_DECODE, (start + 1).astype(np.int32),
+                                              None, d)
+            loc = (self.rows.locate(tasks, start, start + count)
+                   if hasattr(self.rows, "locate") else None)
+            prepared.append(dict(kind=kind, name=name, idx=idx, tasks=tasks, start=start,
+                                 count=count, bt=self._to_device(self._table(rnd, idx)),
+                                 loc=loc, ws=ws))
+        return prepared
+
+    def execute(self, prepared: list, timed: bool = True) -> dict:
+        """Runs prepared rounds' ops.  Rows come from rows.fetch(which, locator) when the
+        source offers `locate`/`fetch` (device-resident rows), else from rows(which, tasks,
+        p0, p1).  Returns {"extend": (op indices, out, lse), "decode": (...)}."""
+        kv, dev = self.kv, self.kv.device
+        d = self.kv.dims
+        result = {}
+        for p in prepared:
+            kind, name, start, count, bt = p["kind"], p["name"], p["start"], p["count"], p["bt"]
+            if p["loc"] is not None:
+                k, v, q = (self.rows.fetch(w, p["loc"]) for w in ("k", "v", "q"))
+            else:
+                k, v, q = (self._up(self.rows(w, p["tasks"], start, start + count))
+                           for w in ("k", "v", "q"))
             out = torch.empty_like(q)
             lse = (torch.empty((q.shape[0], q.shape[1]), dtype=torch.float32, device=dev)
                    if self.with_lse else None)
+            ws = kv.workspace(p["ws"])
             if timed:
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
-            if kind == OP_EXTEND:
-                ws = kv.workspace(max(
-                    _lib.tide_workspace_size(_lib.TIDE_OP_KV_APPEND, start, count, d),
-                    _lib.tide_workspace_size(_lib.TIDE_OP_EXTEND, start, count, d)))
-            else:
-                kv_len = (start + 1).astype(np.int32)
-                ws = kv.workspace(_lib.tide_workspace_size(_lib.TIDE_OP_DECODE, kv_len, None, d))
-            if timed:
                 e0.record()
             if kind == OP_EXTEND:
                 _lib.tide_kv_append(k, v, kv.k_pool, kv.v_pool, bt, start, count, d, ws)
@@ -230,6 +258,7 @@ class Replay:
                     np.sum(pe[1] * pe[0] + pe[1] * (pe[1] + 1) / 2))
             else:
                 # one token per task: the append is fused into the decode call
+                kv_len = (start + 1).astype(np.int32)
                 _lib.tide_decode_append_attn(q, k, v, kv.k_pool, kv.v_pool, bt, kv_len, d, out,
                                              lse, 0, ws)
                 self.kv_bytes += float(np.sum(kv_len)) * d.num_kv_heads * d.head_dim * 4
@@ -238,8 +267,19 @@ class Replay:
                 self._events.append((name, e0, e1))
             self.tokens[name] += int(count.sum())
             self.calls += 1
-            result[name] = (idx, out, lse)
+            result[name] = (p["idx"], out, lse)
         return result
+
+    def reserve(self, prepared_rounds) -> None:
+        """Grows the pool's workspace to what the prepared rounds need, so that no
+        allocation happens while they execute."""
+        need = [p["ws"] for rnd in prepared_rounds for p in rnd]
+        if need:
+            self.kv.workspace(max(need))
+
+    def run(self, rnd: Round, timed: bool = True) -> dict:
+        """prepare + execute of one round."""
+        return self.execute(self.prepare(rnd), timed)
 
     def collect(self):
         """Waits for the queued rounds and adds their stage times."""
