@@ -75,8 +75,9 @@ int task_lengths(int op, int32_t b, const int32_t* lens_a, const int32_t* lens_b
 // choice compares closed-form run-time estimates: the makespan of n workgroups costing
 // c_i tiles each on 256 CUs is max c when n <= 256 (all start at once), and is taken as
 // max(max c, sum c / 256 + max c / 2) otherwise; a tile costs less while few CUs are
-// busy (the clock is higher), and a split plan adds the merge's HBM traffic and launch.  The planner runs on every call, so everything here is linear
-// in the number of blocks, and only the chosen plan is materialised.
+// busy (the clock is higher), and a split plan adds the merge's HBM traffic and launch.
+// The planner runs on every call, so everything here is linear in the number of blocks,
+// and only the chosen plan is materialised.
 namespace {
 
 constexpr int kCus = 256;  // MI355X compute units, 32 per XCD
@@ -97,9 +98,10 @@ struct Block {
   int32_t task, tok0, ntok, ntiles;
 };
 
-// Chunks of a block for chunk length T: about ntiles / T, on a fixed grid [c*T, (c+1)*T)
-// whose last chunk takes the rest (up to 1.5 T), so the same chunk of a unit's blocks
-// covers the same keys.  T == 0: the plain plan (one chunk).
+// Chunks of a block for chunk length T: about ntiles / T (at most kMaxChunks), on a
+// fixed grid [c*T, (c+1)*T) whose last chunk takes the rest (up to 1.5 T below the cap),
+// so the same chunk of a unit's blocks covers the same keys.  T == 0: the plain plan
+// (one chunk).
 inline int32_t num_chunks(int32_t ntiles, int32_t T) {
   if (T <= 0) return 1;
   return (int32_t)std::min<int64_t>(kMaxChunks, std::max<int64_t>(1, (ntiles + T / 2) / T));
