@@ -301,11 +301,13 @@ void decode_split_kernel(DecodeArgs a) {
 // One wave per (task, query head): combine the task's split partials.
 template <int D>
 __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_merge_kernel(DecodeArgs a) {
-  const int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-  if (row >= (int64_t)a.num_tasks * a.num_q_heads) return;
-  const int task = (int)(row / a.num_q_heads);
-  merge_partials<D>(a.part_ml + row * a.max_splits * 4, 4, a.part_o + row * a.max_splits * D, D,
-                    a.tasks[task].aux, a.out + row * D, a.lse ? a.lse + row : nullptr);
+  // wave-uniform and 32-bit (the launch has num_tasks * Hq < 2^31 waves)
+  const int row = (int)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (row >= a.num_tasks * a.num_q_heads) return;
+  const int task = row / a.num_q_heads;
+  const int64_t r = row;
+  merge_partials<D>(a.part_ml + r * a.max_splits * 4, 4, a.part_o + r * a.max_splits * D, D,
+                    a.tasks[task].aux, a.out + r * D, a.lse ? a.lse + r : nullptr);
 }
 
 template <int D, bool kShared, bool kAppend>
@@ -318,6 +320,7 @@ hipError_t launch(const DecodeArgs& a, hipStream_t stream) {
     if (e != hipSuccess) return e;
   }
   const int64_t rows = (int64_t)a.num_tasks * a.num_q_heads;
+  if (rows >= INT32_MAX - kWavesPerBlock) return hipErrorInvalidValue;
   if (rows > 0) {
     const int blocks = (int)((rows + kWavesPerBlock - 1) / kWavesPerBlock);
     hipLaunchKernelGGL((decode_merge_kernel<D>), dim3(blocks), dim3(kWavesPerBlock * 64), 0,

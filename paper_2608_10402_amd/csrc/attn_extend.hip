@@ -473,10 +473,12 @@ constexpr int kMergeWaves = 4;
 // partials; rows that were not split were written by the attention kernel.
 template <int D>
 __global__ __launch_bounds__(kMergeWaves * 64) void extend_merge_kernel(ExtendArgs a) {
-  const int64_t w = (int64_t)blockIdx.x * kMergeWaves + (threadIdx.x >> 6);
-  if (w >= (int64_t)a.total_rows * a.num_q_heads) return;
-  const int row = (int)(w / a.num_q_heads);
-  const int head = (int)(w - (int64_t)row * a.num_q_heads);
+  // wave-uniform and 32-bit (the launch has total_rows * Hq < 2^31 waves)
+  const int wi = (int)blockIdx.x * kMergeWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (wi >= a.total_rows * a.num_q_heads) return;
+  const int row = wi / a.num_q_heads;
+  const int head = wi - row * a.num_q_heads;
+  const int64_t w = wi;
   const MergeRow mr = a.merge_rows[row];
   if (mr.nsplit == 0) return;
   const int64_t s0 = (int64_t)mr.base * a.num_q_heads + head;
@@ -502,6 +504,7 @@ hipError_t launch(const ExtendArgs& a, hipStream_t stream) {
   hipError_t e = launch_attn<D, true>(a, stream);
   if (e != hipSuccess || !a.merge_rows) return e;
   const int64_t waves = (int64_t)a.total_rows * a.num_q_heads;
+  if (waves >= INT32_MAX - kMergeWaves) return hipErrorInvalidValue;
   const int blocks = (int)((waves + kMergeWaves - 1) / kMergeWaves);
   hipLaunchKernelGGL((extend_merge_kernel<D>), dim3(blocks), dim3(kMergeWaves * 64), 0, stream, a);
   return hipGetLastError();

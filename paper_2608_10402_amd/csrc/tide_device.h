@@ -85,6 +85,44 @@ __device__ __forceinline__ void merge_partials(const float* ml, int64_t ml_strid
                                                float* lse_out) {
   const int lane = threadIdx.x & 63;
   constexpr int kPer = D / 64;
+  constexpr int kFew = 16;
+  if (n <= kFew) {
+    // Up to kFew splits: the statistics and every partial this lane needs are loaded
+    // before any arithmetic, so the wave waits for one memory round trip, not two.  The
+    // sums run in the same order as below, so both paths give identical results.
+    f32x4 st = {kNoMax, 0.0f, 0.0f, 0.0f};
+    if (lane < n) st = *reinterpret_cast<const f32x4*>(ml + lane * ml_stride);
+    float src[kFew][kPer];
+#pragma unroll
+    for (int i = 0; i < kFew; ++i)
+#pragma unroll
+      for (int k = 0; k < kPer; ++k)
+        src[i][k] = i < n ? po[(int64_t)i * po_stride + kPer * lane + k] : 0.0f;
+    const float mx = wave_max(st[0]);
+    const float wgt = lane < n ? fast_exp2(st[0] - mx) : 0.0f;
+    float acc[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) acc[k] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kFew; ++i) {
+      if (i >= n) break;
+      const float wi = __shfl(wgt, i, 64);
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) acc[k] += wi * src[i][k];
+    }
+    const float inv = 1.0f / wave_sum(wgt * st[1]);
+    if (kPer == 2) {
+      *reinterpret_cast<uint32_t*>(orow + 2 * lane) = pack_bf16x2(acc[0] * inv, acc[kPer - 1] * inv);
+    } else {
+      const uint32_t w = pack_bf16x2(acc[0] * inv, 0.0f);
+      orow[lane] = (uint16_t)(w & 0xFFFFu);
+    }
+    if (lse_out) {
+      const float l_ex = wave_sum(wgt * st[2]);
+      if (lane == 0) *lse_out = (mx + __log2f(l_ex)) * kLn2;
+    }
+    return;
+  }
   float mx = kNoMax;
   for (int s = lane; s < n; s += 64) mx = fmaxf(mx, ml[s * ml_stride]);
   mx = wave_max(mx);
