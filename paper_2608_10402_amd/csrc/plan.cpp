@@ -443,6 +443,23 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
           items.push_back(it);
         }
     }
+    // Longest first: the shorter last chunks of the tasks then run at the end of the
+    // launch, while the CUs that free up early still find work (the result does not
+    // depend on the order: each split writes its own partial slot).
+    {
+      auto keys = [&](const DecodeItem& x) {
+        return std::min<int64_t>(chunk, (int64_t)tasks[x.task].prefix + 1 - x.k_begin);
+      };
+      std::vector<DecodeItem> tail;  // every task's last, shorter chunk
+      size_t nfull = 0;
+      for (const DecodeItem& it : items) {
+        if (keys(it) == chunk) items[nfull++] = it;
+        else tail.push_back(it);
+      }
+      std::stable_sort(tail.begin(), tail.end(),
+                       [&](const DecodeItem& x, const DecodeItem& y) { return keys(x) > keys(y); });
+      std::copy(tail.begin(), tail.end(), items.begin() + nfull);
+    }
     plan->chunk = (int32_t)chunk;
     plan->max_splits = max_splits;
     n_items = (int64_t)items.size();
