@@ -611,6 +611,12 @@ int make_plan_shared(int32_t num_tasks, const int32_t* kv_lens, int32_t num_grou
         }
     }
   }
+  // Longest first, as for plain decode.  The sort is stable and the items of one prompt
+  // chunk have equal lengths and are adjacent, so they stay adjacent.
+  std::stable_sort(items.begin(), items.end(),
+                   [](const SharedDecodeItem& x, const SharedDecodeItem& y) {
+                     return x.k_end - x.k_begin > y.k_end - y.k_begin;
+                   });
   if ((int64_t)items.size() > INT32_MAX / 4) return TIDE_ERR_INVALID_ARG;
   plan->chunk = (int32_t)chunk;
   plan->max_splits = max_splits;
