@@ -84,6 +84,9 @@ def parse_args():
     ap.add_argument("--workload", default="agent_resume_7b")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall-time budget of the oracle CPU baseline sample (0 disables it)")
+    ap.add_argument("--one-task", type=int, default=1,
+                    help="for extend workloads, also time a one-task resume outside the step "
+                         "(1) or not (0; profiling runs use 0 so every launch is the step's)")
     ap.add_argument("--reprefill", type=int, default=1,
                     help="include the recompute comparison (append history + full prefill) "
                          "for extend workloads (1) or not (0)")
@@ -552,7 +555,8 @@ def main():
         rooflines["extend"] = {"bound": "mfma", "achieved": round(v, 2), "peak": PEAK_BF16_TFLOPS,
                                "unit": "TFLOP/s", "frac": round(v / PEAK_BF16_TFLOPS, 4)}
         extra["extend_tokens_per_s"] = round(float(wl.extend_lens.sum()) / (t * 1e-3), 1)
-        extra["one_task_resume"] = one_task_resume(wl, kv, keep, args.steps, torch, stream)
+        if args.one_task:
+            extra["one_task_resume"] = one_task_resume(wl, kv, keep, args.steps, torch, stream)
     if "prefill" in ms:
         t, f, _ = total("prefill")
         v = f / (t * 1e-3) / 1e12
