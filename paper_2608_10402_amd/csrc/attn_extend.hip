@@ -62,13 +62,6 @@ struct ES {
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
-typedef const __attribute__((address_space(4))) int32_t const_i32;
-
-// Block-table word `idx` of a row, read through the constant address space: the table is
-// read-only during the kernel, so a wave-uniform index becomes a scalar load.
-__device__ __forceinline__ int32_t load_page_id(const int32_t* row, int idx) {
-  return ((const_i32*)row)[idx];
-}
 
 // 16 bytes per lane from `page` (a buffer of `bytes` bytes; reads past it return 0) at
 // byte offset `voff`, written by the buffer unit straight into LDS at lds + 16 * lane.

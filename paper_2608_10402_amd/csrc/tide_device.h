@@ -25,6 +25,15 @@ constexpr float kNoMax = -1.0e30f;
 // and the accumulator rescale is skipped on almost every tile.
 constexpr float kRescaleSlack = 8.0f;
 
+typedef const __attribute__((address_space(4))) int32_t const_i32;
+
+// Block-table word `idx` of a row, read through the constant address space: the table is
+// read-only during a kernel, so a wave-uniform index becomes a scalar load (counted by
+// lgkmcnt, so waiting for it never waits for outstanding vector loads).
+__device__ __forceinline__ int32_t load_page_id(const int32_t* row, int idx) {
+  return ((const_i32*)row)[idx];
+}
+
 __device__ __forceinline__ u32x4 load_u32x4(const void* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
