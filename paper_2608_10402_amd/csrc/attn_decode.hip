@@ -129,8 +129,9 @@ __device__ __forceinline__ uint2 keep_first4(uint2 x, int n) {
 // loaded once for all of them), or a task's own keys after it.  Otherwise DecodeItem.
 // kAppend (plain items only): the newest token of each task (position kv_len - 1) is not
 // in the pool yet.  The split that holds it first writes that token's K/V from
-// a.k_new / a.v_new into its pool slot, waits for the stores, then reads as usual.  No
-// other split reads that slot, so the result equals appending first and then decoding.
+// a.k_new / a.v_new into its pool slot, and waits for the stores before it issues the
+// loads of the step that holds the slot.  No other split reads that slot, so the result
+// equals appending first and then decoding.
 template <int D, bool kShared, bool kAppend>
 __global__ __launch_bounds__(kWavesPerBlock * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void decode_split_kernel(DecodeArgs a) {
@@ -194,21 +195,34 @@ void decode_split_kernel(DecodeArgs a) {
   const uint32_t v_off = (uint32_t)(col * kPage * 2 + 8 * grp);    // head-dim row `col`
 
   // Page ids come from scalar loads, so that no wait for one ever waits for the K/V
-  // loads in flight.  Pages past the context (and invalid ids) read page 0, which the
-  // masks below keep out of the result; an invalid id is reported once, at the end.
+  // loads in flight.  A page past the context (or with an invalid id) gets a buffer
+  // descriptor of range 0: its loads return zeros without touching memory, and the
+  // masks below keep those slots out of the result.  An invalid id is reported once, at
+  // the end.
   bool flag_error = false;
-  auto page_block = [&](int lp) -> int64_t {
+  auto page_ref = [&](int lp, int64_t& blk) -> int {
     const bool in = lp < npages;
     const int32_t p = load_page_id(bt_row, in ? lp : npages - 1);
     const bool bad = p < 0 || p >= a.num_pages;
     if (bad && in) flag_error = true;
-    return ((int64_t)(bad || !in ? 0 : p) * a.num_kv_heads + kv_h) * kBlk;
+    const bool use = in && !bad;
+    blk = ((int64_t)(use ? p : 0) * a.num_kv_heads + kv_h) * kBlk;
+    return use ? (int)kBlk : 0;
   };
+  // the split that appends the newest token (kAppend)
+  const bool appender = kAppend && kend == kv_len;
   auto load = [&](DecodeRegs<D>& r, uint8_t* kbuf, int k, auto policy_tag) {
-    const int64_t b0 = page_block(k / kPage), b1 = page_block(k / kPage + 1);
+    if (kAppend && appender && k + kDecodeStep >= kv_len) {
+      // this step holds the appended slot: its stores must have completed first
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0) expcnt(0) lgkmcnt(0)
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);  // and no load is moved above the wait
+    }
+    int64_t b0, b1;
+    const int n0 = page_ref(k / kPage, b0), n1 = page_ref(k / kPage + 1, b1);
     load_step<D, decltype(policy_tag)::value>(
-        r, kbuf, block_rsrc(kpool + b0, (int)kBlk), block_rsrc(kpool + b1, (int)kBlk),
-        block_rsrc(vpool + b0, (int)kBlk), block_rsrc(vpool + b1, (int)kBlk), k_src, v_off);
+        r, kbuf, block_rsrc(kpool + b0, n0), block_rsrc(kpool + b1, n1),
+        block_rsrc(vpool + b0, n0), block_rsrc(vpool + b1, n1), k_src, v_off);
   };
 
   f32x4 o[D / 16];
@@ -281,11 +295,13 @@ void decode_split_kernel(DecodeArgs a) {
 
   if constexpr (kAppend) {
     // The split that ends the context appends its newest token before reading: K row
-    // and V^T column of slot pos % 16, then waits until the stores have completed, so
-    // the loads below return them.  No other wave reads this page (splits end on
-    // 32-key boundaries), and no earlier load in this kernel can have put a stale copy
-    // of it in this CU's L1.
-    if (kend == kv_len) {
+    // and V^T column of slot pos % 16.  Its loads of earlier steps overlap the stores;
+    // the step that holds the slot waits for them (in `load`), so its loads return the
+    // new token.  No other wave reads this page (splits end on 32-key boundaries, other
+    // kv heads' blocks are whole 4 KB pages, and pages past a context are never read),
+    // and this wave's earlier steps read earlier pages, so no load in this kernel can
+    // have put a stale copy of the slot in this CU's L1.
+    if (appender) {
       const int pos = kv_len - 1, slot = pos % kPage;
       const int32_t p = bt_row[pos / kPage];
       if (p >= 0 && p < a.num_pages) {
@@ -301,8 +317,6 @@ void decode_split_kernel(DecodeArgs a) {
       } else {
         flag_error = true;
       }
-      __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0) expcnt(0) lgkmcnt(0): stores done
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);  // and no load is moved above them
     }
   }
 
