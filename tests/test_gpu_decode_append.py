@@ -18,9 +18,24 @@ from gpu_harness import (DeviceWorkload, assert_close, assert_lse, dev_bf16, hos
 pytestmark = pytest.mark.gpu
 S = W.SPECS
 
+def _newest_token_on_page0():
+    """Task 0's newest token lands on physical page 0, and every task's context ends in
+    the first page of its last 32-key step, so the second page of that step lies past
+    the context.  Such pages are never read (a zero-range load), so no wave can bring a
+    copy of page 0 into its CU's L1 before the fused append writes it."""
+    wl = W.custom_workload(16, 4, 128, [40, 100, 7, 200, 0, 72, 136, 1000, 520], [1] * 9,
+                           seed=24)
+    assert ((wl.seq_lens % 32 >= 1) & (wl.seq_lens % 32 <= 16)).all()
+    p = int(wl.block_table[0, (wl.seq_lens[0] - 1) // 16])
+    perm = np.arange(wl.num_pages, dtype=np.int32)
+    perm[p], perm[0] = 0, p
+    return wl.remap_pages(perm)
+
+
 # contexts (including the decoded token): 1 (the token is the whole context), 16 (last
 # slot of the first page), 17 (first slot of the second page), 32, 33, 2049; GQA 1..16
 CASES = {
+    "newest_on_page0": _newest_token_on_page0,
     "resumed_decode_small": lambda: W.make_workload(S["resumed_decode"].shrunk(12, 16)),
     "edges_g4_d128": lambda: W.custom_workload(16, 4, 128, [0, 15, 16, 31, 32, 2048, 100],
                                                [1] * 7, seed=21),
