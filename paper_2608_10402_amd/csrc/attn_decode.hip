@@ -26,9 +26,10 @@
 //     rows of page t are its token slots, so each lane's probabilities are exactly those
 //     slots and P never moves between lanes.
 //   * Every load instruction reads one page: the page block is a scalar base, lanes add
-//     a fixed offset.  Page ids arrive 64 at a time (one vector load, then readlane).
+//     a fixed offset.  Page ids come from scalar loads.
 //   * Two buffers in ping-pong (LDS for K, registers for V) keep the next 32-key step in
-//     flight; at most 256 registers so two waves share each SIMD.
+//     flight; at most 256 registers and 64 KB of LDS per 4-wave block, so two waves share
+//     each SIMD.
 //   * Partial (o, m, l) per split go to the workspace; a second small kernel merges them.
 #include <type_traits>
 

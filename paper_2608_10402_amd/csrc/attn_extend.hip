@@ -186,21 +186,25 @@ void extend_attn_kernel(ExtendArgs a) {
                         : (uint32_t)(r * S::kRowBytes + kswz<D>(r, lane % S::kNG) * 16);
   }
   bool bad_page = false;
-  // Page id of this wave's page of `tile` (a scalar load); pages past the sequence are
-  // read from page 0, which always exists: their keys are masked, their V zeroed.
-  auto page_word = [&](int tile) -> int32_t {
+  // Page id of this wave's page of `tile` (a scalar load), or kPastEnd for a page past
+  // the sequence (a value no page id can take).
+  constexpr int64_t kPastEnd = -(int64_t(1) << 40);
+  auto page_word = [&](int tile) -> int64_t {
     const int lp = (tbase + tile) * 4 + pw;
-    return lp < npages ? load_page_id(bt, lp) : 0;
+    return lp < npages ? (int64_t)load_page_id(bt, lp) : kPastEnd;
   };
   // Every step issues the same number of loads on every wave, so the vmcnt waits below
-  // hold on every path; a tile past the item (live == false) is read through a
-  // zero-length buffer, which returns zeros without touching memory.
-  auto stream_tile = [&](int32_t word, uint8_t* kv, bool live) {
-    const bool bad = live && (word < 0 || (int64_t)word >= a.num_pages);
+  // hold on every path.  A tile past the item (live == false), a page past the sequence
+  // and an invalid page id are read through a zero-length buffer, which returns zeros
+  // without touching memory; their keys are masked and their V slots zeroed.
+  auto stream_tile = [&](int64_t word, uint8_t* kv, bool live) {
+    const bool past = word == kPastEnd;
+    const bool bad = live && !past && (word < 0 || word >= a.num_pages);
     bad_page |= bad;
-    const int64_t blk = ((bad ? 0 : (int64_t)word) * a.num_kv_heads + it.kv_head) *
+    const bool use = live && !past && !bad;
+    const int64_t blk = ((use ? word : 0) * a.num_kv_heads + it.kv_head) *
                         (int64_t)S::kPageBytes;
-    const int bytes = live ? S::kPageBytes : 0;
+    const int bytes = use ? S::kPageBytes : 0;
 #pragma unroll
     for (int i = 0; i < S::kDma; ++i)
       dma16(src_pool + blk, bytes, src_off[i], kv + lds_half + pw * S::kPageBytes + i * 1024);
@@ -224,7 +228,7 @@ void extend_attn_kernel(ExtendArgs a) {
   stream_tile(page_word(1), kv_lds1, ntiles > 1);
   __builtin_amdgcn_sched_barrier(0);
   stream_tile(page_word(2), kv_lds2, ntiles > 2);
-  int32_t next_word = page_word(3);  // page id of the next tile to stream
+  int64_t next_word = page_word(3);  // page id of the next tile to stream
   wait_vmem<2 * S::kDma>();          // tile 0 (and the query rows) landed
   phase_barrier();
   if (v_half) phase_barrier();  // waves 4-7 start one phase behind
