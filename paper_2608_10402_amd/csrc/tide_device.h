@@ -150,12 +150,22 @@ __device__ __forceinline__ void merge_partials(const float* ml, int64_t ml_strid
       l_ex += wgt * st[2];
     }
     const int cnt = min(64, n - s0);
-#pragma unroll 4
-    for (int i = 0; i < cnt; ++i) {
-      const float wi = __shfl(wgt, i, 64);
-      const float* src = po + (int64_t)(s0 + i) * po_stride + kPer * lane;
+    // kFew partials at a time, all loaded before they are summed (in split order)
+    for (int i0 = 0; i0 < cnt; i0 += kFew) {
+      float src[kFew][kPer];
 #pragma unroll
-      for (int k = 0; k < kPer; ++k) acc[k] += wi * src[k];
+      for (int i = 0; i < kFew; ++i)
+#pragma unroll
+        for (int k = 0; k < kPer; ++k)
+          src[i][k] = i0 + i < cnt ? po[(int64_t)(s0 + i0 + i) * po_stride + kPer * lane + k]
+                                   : 0.0f;
+#pragma unroll
+      for (int i = 0; i < kFew; ++i) {
+        if (i0 + i >= cnt) break;
+        const float wi = __shfl(wgt, i0 + i, 64);
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) acc[k] += wi * src[i][k];
+      }
     }
   }
   l_round = wave_sum(l_round);

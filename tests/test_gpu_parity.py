@@ -146,7 +146,7 @@ def dcase(request):
     return name, wl, dw, q, ref, ref_lse
 
 
-@pytest.mark.parametrize("splits", [0, 1, 2, 7, 64])
+@pytest.mark.parametrize("splits", [0, 1, 2, 7, 64, 100])
 def test_decode_parity(dcase, splits):
     name, wl, dw, q, ref, ref_lse = dcase
     qd = dev_bf16(q)
