@@ -28,8 +28,9 @@
 //   * Every load instruction reads one page: the page block is a scalar base, lanes add
 //     a fixed offset.  Page ids come from scalar loads.
 //   * Two buffers in ping-pong (LDS for K, registers for V) keep the next 32-key step in
-//     flight; at most 256 registers and 64 KB of LDS per 4-wave block, so two waves share
-//     each SIMD.
+//     flight; at most 256 registers and 16 KB of LDS per wave, so two waves share each
+//     SIMD.  A workgroup of 8 waves takes 8 consecutive items (all kv heads of one task's
+//     chunk, whose pages are contiguous) onto one CU.
 //   * Partial (o, m, l) per split go to the workspace; a second small kernel merges them.
 #include <type_traits>
 
@@ -39,7 +40,7 @@
 namespace tide {
 namespace kern {
 
-constexpr int kWavesPerBlock = 4;
+constexpr int kWavesPerBlock = 8;
 
 // V^T operands of one 32-key step (pages p0 = keys k..k+15 and p1 = k+16..k+31):
 //   v[t][h]: head-dim tile t, slots 4*grp..4*grp+3 of page h.
