@@ -425,7 +425,7 @@ def run_ctb(args, torch, tide):
     ctb = res["ctb"]
     v = ctb["decode_GBps"]
     roofline = {"bound": "hbm", "achieved": v, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(v / PEAK_HBM_GBS, 4), "kernel": "decode_split_kernel<128, false, true>",
+                "frac": round(v / PEAK_HBM_GBS, 4), "kernel": "decode_split_kernel<128, false, true, 4|8>",
                 "traffic": None}
     extra = {"policies": res, "setup_s": round(setup_s, 1),
              "attention_speedup_ctb_vs_request_f1024": round(
@@ -612,8 +612,8 @@ def main():
                "shared_decode" if "shared_decode" in rooflines else "decode")
     roofline = dict(rooflines[primary])
     roofline["kernel"] = {"extend": "extend_attn_kernel<128, false, false>",
-                          "decode": "decode_split_kernel<128, false, false>",
-                          "shared_decode": "decode_split_kernel<128, true, false>"}[primary]
+                          "decode": "decode_split_kernel<128, false, false, 8>",
+                          "shared_decode": "decode_split_kernel<128, true, false, 8>"}[primary]
     roofline["traffic"] = counter_traffic(s.key, primary)
 
     cpu = None

@@ -29,8 +29,8 @@
 //     a fixed offset.  Page ids come from scalar loads.
 //   * Two buffers in ping-pong (LDS for K, registers for V) keep the next 32-key step in
 //     flight; at most 256 registers and 16 KB of LDS per wave, so two waves share each
-//     SIMD.  A workgroup of 8 waves takes 8 consecutive items (all kv heads of one task's
-//     chunk, whose pages are contiguous) onto one CU.
+//     SIMD.  A large launch runs 8-wave workgroups (8 consecutive items onto one CU), a
+//     small one 4-wave workgroups.
 //   * Partial (o, m, l) per split go to the workspace; a second small kernel merges them.
 #include <type_traits>
 
@@ -40,7 +40,13 @@
 namespace tide {
 namespace kern {
 
-constexpr int kWavesPerBlock = 8;
+// Waves per workgroup of the split kernel: 8 consecutive items (at 8 kv heads, all heads
+// of one task's chunk, whose page blocks are contiguous) on one CU when the launch has
+// enough items to give every CU a full workgroup; otherwise 4, so that a small launch
+// still spreads over all CUs (a 4-wave workgroup takes half a CU's LDS).
+constexpr int kBigWaves = 8, kSmallWaves = 4;
+constexpr int kBigLaunchItems = 2048;  // 256 CUs x 8 waves
+constexpr int kMergeWaves = 4;
 
 // V^T operands of one 32-key step (pages p0 = keys k..k+15 and p1 = k+16..k+31):
 //   v[t][h]: head-dim tile t, slots 4*grp..4*grp+3 of page h.
@@ -134,18 +140,18 @@ __device__ __forceinline__ uint2 keep_first4(uint2 x, int n) {
 // a.k_new / a.v_new into its pool slot, and waits for the stores before it issues the
 // loads of the step that holds the slot.  No other split reads that slot, so the result
 // equals appending first and then decoding.
-template <int D, bool kShared, bool kAppend>
-__global__ __launch_bounds__(kWavesPerBlock * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+template <int D, bool kShared, bool kAppend, int kWaves>
+__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void decode_split_kernel(DecodeArgs a) {
   const int lane = threadIdx.x & 63;
   // the wave index is uniform across the wave: say so, so the item and every address
   // derived from it stay scalar
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int item_id = blockIdx.x * kWavesPerBlock + wave;
+  const int item_id = blockIdx.x * kWaves + wave;
   // K pages of the two steps in flight, one region per wave (2 pages per step)
   using L = KLds<D>;
-  __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[kWavesPerBlock * 2 * L::kPageBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t k_lds1[kWavesPerBlock * 2 * L::kPageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t k_lds0[kWaves * 2 * L::kPageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t k_lds1[kWaves * 2 * L::kPageBytes];
   if (item_id >= a.num_items) return;  // whole wave exits; no block-level barrier below
   int first_task, ntasks, kv_head, split, kbeg, kend;
   if constexpr (kShared) {
@@ -380,9 +386,9 @@ void decode_split_kernel(DecodeArgs a) {
 
 // One wave per (task, query head): combine the task's split partials.
 template <int D>
-__global__ __launch_bounds__(kWavesPerBlock * 64) void decode_merge_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kMergeWaves * 64) void decode_merge_kernel(DecodeArgs a) {
   // wave-uniform and 32-bit (the launch has num_tasks * Hq < 2^31 waves)
-  const int row = (int)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int row = (int)blockIdx.x * kMergeWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (row >= a.num_tasks * a.num_q_heads) return;
   const int task = row / a.num_q_heads;
   const int64_t r = row;
@@ -393,30 +399,42 @@ __global__ __launch_bounds__(kWavesPerBlock * 64) void decode_merge_kernel(Decod
 template <int D, bool kShared, bool kAppend>
 hipError_t launch(const DecodeArgs& a, hipStream_t stream) {
   if (a.num_items > 0) {
-    const int blocks = (a.num_items + kWavesPerBlock - 1) / kWavesPerBlock;
-    hipLaunchKernelGGL((decode_split_kernel<D, kShared, kAppend>), dim3(blocks),
-                       dim3(kWavesPerBlock * 64), 0, stream, a);
+    if (a.num_items >= kBigLaunchItems) {
+      const int blocks = (a.num_items + kBigWaves - 1) / kBigWaves;
+      hipLaunchKernelGGL((decode_split_kernel<D, kShared, kAppend, kBigWaves>), dim3(blocks),
+                         dim3(kBigWaves * 64), 0, stream, a);
+    } else {
+      const int blocks = (a.num_items + kSmallWaves - 1) / kSmallWaves;
+      hipLaunchKernelGGL((decode_split_kernel<D, kShared, kAppend, kSmallWaves>), dim3(blocks),
+                         dim3(kSmallWaves * 64), 0, stream, a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   const int64_t rows = (int64_t)a.num_tasks * a.num_q_heads;
-  if (rows >= INT32_MAX - kWavesPerBlock) return hipErrorInvalidValue;
+  if (rows >= INT32_MAX - kMergeWaves) return hipErrorInvalidValue;
   if (rows > 0) {
-    const int blocks = (int)((rows + kWavesPerBlock - 1) / kWavesPerBlock);
-    hipLaunchKernelGGL((decode_merge_kernel<D>), dim3(blocks), dim3(kWavesPerBlock * 64), 0,
+    const int blocks = (int)((rows + kMergeWaves - 1) / kMergeWaves);
+    hipLaunchKernelGGL((decode_merge_kernel<D>), dim3(blocks), dim3(kMergeWaves * 64), 0,
                        stream, a);
   }
   return hipGetLastError();
 }
 
-// Both variants of each head size are instantiated explicitly: the host pass otherwise
-// emits the launch stub of only one of two specialisations that differ in the bool.
-template __global__ void decode_split_kernel<128, false, false>(DecodeArgs);
-template __global__ void decode_split_kernel<128, true, false>(DecodeArgs);
-template __global__ void decode_split_kernel<128, false, true>(DecodeArgs);
-template __global__ void decode_split_kernel<64, false, false>(DecodeArgs);
-template __global__ void decode_split_kernel<64, true, false>(DecodeArgs);
-template __global__ void decode_split_kernel<64, false, true>(DecodeArgs);
+// Every variant of each head size is instantiated explicitly: the host pass otherwise
+// emits the launch stub of only one of two specialisations that differ in a bool.
+template __global__ void decode_split_kernel<128, false, false, kBigWaves>(DecodeArgs);
+template __global__ void decode_split_kernel<128, false, false, kSmallWaves>(DecodeArgs);
+template __global__ void decode_split_kernel<128, true, false, kBigWaves>(DecodeArgs);
+template __global__ void decode_split_kernel<128, true, false, kSmallWaves>(DecodeArgs);
+template __global__ void decode_split_kernel<128, false, true, kBigWaves>(DecodeArgs);
+template __global__ void decode_split_kernel<128, false, true, kSmallWaves>(DecodeArgs);
+template __global__ void decode_split_kernel<64, false, false, kBigWaves>(DecodeArgs);
+template __global__ void decode_split_kernel<64, false, false, kSmallWaves>(DecodeArgs);
+template __global__ void decode_split_kernel<64, true, false, kBigWaves>(DecodeArgs);
+template __global__ void decode_split_kernel<64, true, false, kSmallWaves>(DecodeArgs);
+template __global__ void decode_split_kernel<64, false, true, kBigWaves>(DecodeArgs);
+template __global__ void decode_split_kernel<64, false, true, kSmallWaves>(DecodeArgs);
 
 }  // namespace kern
 
