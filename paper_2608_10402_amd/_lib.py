@@ -146,6 +146,46 @@ def _ws(workspace):
     return workspace.data_ptr(), workspace.numel() * workspace.element_size()
 
 
+def _same_device(*tensors):
+    """All device tensors of one call must live on one device (the pointers are handed to
+    kernels launched on that device)."""
+    devs = {t.device for t in tensors if isinstance(t, torch.Tensor)}
+    if len(devs) > 1:
+        raise ValueError("all tensors of a call must be on one device, got %s" % sorted(map(str, devs)))
+
+
+def _rows(t, name, rows, heads, d):
+    """t must be [rows][heads][d] (the library reads and writes exactly that many bytes).
+    rows None: the lengths are invalid, which the library itself rejects before any device
+    work."""
+    if t is None or rows is None:
+        return
+    if tuple(t.shape) != (rows, heads, d):
+        raise ValueError("%s must have shape (%d, %d, %d), got %s"
+                         % (name, rows, heads, d, tuple(t.shape)))
+
+
+def _lse(t, rows, heads):
+    if t is not None and rows is not None and tuple(t.shape) != (rows, heads):
+        raise ValueError("lse must have shape (%d, %d), got %s" % (rows, heads, tuple(t.shape)))
+
+
+def _block_table(bt, num_tasks):
+    if not isinstance(bt, torch.Tensor) or bt.dim() != 2:
+        raise ValueError("block_table must be a 2-D tensor [num_tasks][bt_stride]")
+    if bt.shape[0] < num_tasks or bt.shape[1] < 1:
+        raise ValueError("block_table has %d rows for %d tasks" % (bt.shape[0], num_tasks))
+    return int(bt.shape[1])
+
+
+def _lens_total(lens):
+    """Sum of a host length array (the row count the library will use), or None when a
+    length is negative: the library returns TIDE_ERR_INVALID_ARG for that itself."""
+    if lens is None or (lens < 0).any():
+        return None
+    return int(lens.astype(np.int64).sum())
+
+
 def _pool_shape(k_pool, v_pool, dims):
     if k_pool.dim() != 4 or v_pool.dim() != 4:
         raise ValueError("pools must be 4-D")
@@ -177,6 +217,13 @@ def tide_kv_append(k_new, v_new, k_pool, v_pool, block_table, prefix_lens, exten
     num_pages = _pool_shape(k_pool, v_pool, dims)
     p, p_p = _host(prefix_lens, "prefix_lens")
     e, e_p = _host(extend_lens, "extend_lens")
+    if p is None or e is None or p.size != e.size:
+        raise ValueError("prefix_lens and extend_lens must have one entry per task")
+    rows = _lens_total(e)
+    _rows(k_new, "k_new", rows, dims.num_kv_heads, dims.head_dim)
+    _rows(v_new, "v_new", rows, dims.num_kv_heads, dims.head_dim)
+    _block_table(block_table, int(p.size))
+    _same_device(k_new, v_new, k_pool, v_pool, block_table, workspace)
     ws, ws_n = _ws(workspace)
     _check(load().tide_kv_append(
         _dev(k_new, torch.bfloat16, "k_new"), _dev(v_new, torch.bfloat16, "v_new"),
@@ -190,6 +237,14 @@ def tide_extend_attn(q, k_pool, v_pool, block_table, prefix_lens, extend_lens, d
     num_pages = _pool_shape(k_pool, v_pool, dims)
     p, p_p = _host(prefix_lens, "prefix_lens")
     e, e_p = _host(extend_lens, "extend_lens")
+    if p is None or e is None or p.size != e.size:
+        raise ValueError("prefix_lens and extend_lens must have one entry per task")
+    rows = _lens_total(e)
+    _rows(q, "q", rows, dims.num_q_heads, dims.head_dim)
+    _rows(out, "out", rows, dims.num_q_heads, dims.head_dim)
+    _lse(lse, rows, dims.num_q_heads)
+    _block_table(block_table, int(p.size))
+    _same_device(q, k_pool, v_pool, block_table, out, lse, workspace)
     ws, ws_n = _ws(workspace)
     _check(load().tide_extend_attn(
         _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"),
@@ -200,10 +255,22 @@ def tide_extend_attn(q, k_pool, v_pool, block_table, prefix_lens, extend_lens, d
         "tide_extend_attn")
 
 
+def _decode_checks(q, out, lse, block_table, kv, dims, *others):
+    if kv is None:
+        raise ValueError("kv_lens is required")
+    n = int(kv.size)
+    _rows(q, "q", n, dims.num_q_heads, dims.head_dim)
+    _rows(out, "out", n, dims.num_q_heads, dims.head_dim)
+    _lse(lse, n, dims.num_q_heads)
+    _block_table(block_table, n)
+    _same_device(q, out, lse, block_table, *others)
+
+
 def tide_decode_attn(q, k_pool, v_pool, block_table, kv_lens, dims: tide_dims, out, lse=None,
                      num_splits: int = 0, workspace=None, stream=None) -> None:
     num_pages = _pool_shape(k_pool, v_pool, dims)
     kv, kv_p = _host(kv_lens, "kv_lens")
+    _decode_checks(q, out, lse, block_table, kv, dims, k_pool, v_pool, workspace)
     ws, ws_n = _ws(workspace)
     _check(load().tide_decode_attn(
         _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"),
@@ -219,6 +286,9 @@ def tide_decode_append_attn(q, k_new, v_new, k_pool, v_pool, block_table, kv_len
                             workspace=None, stream=None) -> None:
     num_pages = _pool_shape(k_pool, v_pool, dims)
     kv, kv_p = _host(kv_lens, "kv_lens")
+    _decode_checks(q, out, lse, block_table, kv, dims, k_pool, v_pool, k_new, v_new, workspace)
+    _rows(k_new, "k_new", int(kv.size), dims.num_kv_heads, dims.head_dim)
+    _rows(v_new, "v_new", int(kv.size), dims.num_kv_heads, dims.head_dim)
     ws, ws_n = _ws(workspace)
     _check(load().tide_decode_append_attn(
         _dev(q, torch.bfloat16, "q"), _dev(k_new, torch.bfloat16, "k_new"),
@@ -255,6 +325,7 @@ def tide_decode_attn_shared(q, k_pool, v_pool, block_table, kv_lens, group_start
     num_pages = _pool_shape(k_pool, v_pool, dims)
     kv, kv_p = _host(kv_lens, "kv_lens")
     ng, gs, gs_p, sh, sh_p = _groups(group_start, shared_lens)
+    _decode_checks(q, out, lse, block_table, kv, dims, k_pool, v_pool, workspace)
     ws, ws_n = _ws(workspace)
     _check(load().tide_decode_attn_shared(
         _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"),
@@ -269,6 +340,14 @@ def tide_full_prefill_attn(q, k_pool, v_pool, block_table, seq_lens, dims: tide_
                            lse=None, workspace=None, stream=None) -> None:
     num_pages = _pool_shape(k_pool, v_pool, dims)
     s, s_p = _host(seq_lens, "seq_lens")
+    if s is None:
+        raise ValueError("seq_lens is required")
+    rows = _lens_total(s)
+    _rows(q, "q", rows, dims.num_q_heads, dims.head_dim)
+    _rows(out, "out", rows, dims.num_q_heads, dims.head_dim)
+    _lse(lse, rows, dims.num_q_heads)
+    _block_table(block_table, int(s.size))
+    _same_device(q, k_pool, v_pool, block_table, out, lse, workspace)
     ws, ws_n = _ws(workspace)
     _check(load().tide_full_prefill_attn(
         _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"),

@@ -250,3 +250,41 @@ def test_shared_decode_rejects_before_gpu():
     rc = lib.tide_decode_attn_shared(None, None, None, 10, None, 4, 0, None, 0, None, None,
                                      ctypes.byref(dims), 0, None, None, None, 0, None)
     assert rc == tide.TIDE_OK  # no tasks: nothing to do
+
+
+# ---- binding: shapes are checked before the C call --------------------------------------------
+def test_binding_checks_row_counts_before_the_call():
+    """The C ABI takes no buffer sizes, so the binding checks every tensor against the host
+    lengths first; a mismatch is a ValueError naming the tensor, never a device access.
+    (Host tensors of the right shape would be rejected next, for not being on a device.)"""
+    import torch
+    dims = _lib.make_dims(8, 2, 64, 0.125)
+    kp = torch.zeros(10, 2, 16, 64, dtype=torch.bfloat16)
+    vp = torch.zeros(10, 2, 64, 16, dtype=torch.bfloat16)
+    bt = torch.zeros(2, 4, dtype=torch.int32)
+    q = torch.zeros(7, 8, 64, dtype=torch.bfloat16)    # 3 + 4 rows
+    with pytest.raises(ValueError, match="q must have shape"):
+        tide.tide_extend_attn(q[:6], kp, vp, bt, [5, 9], [3, 4], dims, q)
+    with pytest.raises(ValueError, match="out must have shape"):
+        tide.tide_extend_attn(q, kp, vp, bt, [5, 9], [3, 4], dims, q[:5])
+    with pytest.raises(ValueError, match="lse must have shape"):
+        tide.tide_extend_attn(q, kp, vp, bt, [5, 9], [3, 4], dims, q,
+                              lse=torch.zeros(7, 4, dtype=torch.float32))
+    with pytest.raises(ValueError, match="block_table has 1 rows"):
+        tide.tide_extend_attn(q, kp, vp, bt[:1], [5, 9], [3, 4], dims, q)
+    with pytest.raises(ValueError, match="q must have shape"):
+        tide.tide_full_prefill_attn(q, kp, vp, bt, [3, 5], dims, q)
+    kn = torch.zeros(7, 2, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="v_new must have shape"):
+        tide.tide_kv_append(kn, kn[:, :1], kp, vp, bt, [5, 9], [3, 4], dims, None)
+    with pytest.raises(ValueError, match="one entry per task"):
+        tide.tide_kv_append(kn, kn, kp, vp, bt, [5, 9, 1], [3, 4], dims, None)
+    qd = torch.zeros(2, 8, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="q must have shape"):
+        tide.tide_decode_attn(qd[:1], kp, vp, bt, [6, 10], dims, qd)
+    with pytest.raises(ValueError, match="k_new must have shape"):
+        tide.tide_decode_append_attn(qd, kn, kn[:2], kp, vp, bt, [6, 10], dims, qd)
+    with pytest.raises(ValueError, match="block_table has 2 rows"):
+        tide.tide_decode_attn_shared(torch.zeros(3, 8, 64, dtype=torch.bfloat16), kp, vp, bt,
+                                     [6, 10, 7], [0, 3], [0], dims,
+                                     torch.zeros(3, 8, 64, dtype=torch.bfloat16))
