@@ -70,9 +70,11 @@
  * Calls enqueue work on `stream` and return without synchronizing (except under
  * TIDE_DEBUG_CHECKS=1).  Device faults surface at the caller's next synchronization.
  * No C++ exception or abort crosses this interface.  The library never allocates
- * device memory; it keeps a small pinned, device-mapped host staging ring (created
- * lazily, released by tide_shutdown) from which a copy kernel on `stream` moves each
- * call's work list into the workspace.  Calls are thread-safe.
+ * device memory at run time (its one static device array, the scratch of
+ * tide_decode_attn_noalloc, comes with the code object); it keeps a small pinned,
+ * device-mapped host staging ring (created lazily, released by tide_shutdown) from which
+ * a copy kernel on `stream` moves each call's work list into the workspace.  Calls that
+ * take a workspace are thread-safe when each call in flight has its own workspace.
  */
 #ifndef TIDE_H_
 #define TIDE_H_
@@ -203,6 +205,25 @@ TIDE_API int tide_decode_append_attn(const void* q, const void* k_new, const voi
                             const int32_t* kv_lens, const tide_dims* dims, int32_t num_splits,
                             void* out, float* lse, void* workspace, size_t workspace_bytes,
                             void* stream);
+
+/*
+ * Decode attention that allocates nothing, for callers that cannot allocate device or
+ * pinned memory: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, result and errors as tide_decode_attn, without the
+ * workspace: the work list and split partials live in a static device array of
+ * TIDE_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on until the
+ * process ends.  A call whose tide_workspace_size(TIDE_OP_DECODE, ...) exceeds that
+ * returns TIDE_ERR_CAPACITY before any device work.  The work list is copied into the
+ * array with hipMemcpyAsync from pageable host memory, so the call may wait for work
+ * already queued on `stream`.  Every call on one GPU uses the same array: two calls in
+ * flight at once on one GPU (on different streams, or from different threads) race and
+ * give undefined results; serialize them on one stream.
+ */
+#define TIDE_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+TIDE_API int tide_decode_attn_noalloc(const void* q, const void* k_pool, const void* v_pool,
+                             int64_t num_pages, const int32_t* block_table, int32_t bt_stride,
+                             int32_t num_tasks, const int32_t* kv_lens, const tide_dims* dims,
+                             int32_t num_splits, void* out, float* lse, void* stream);
 
 /*
  * Decode attention for tasks grouped by a shared prompt prefix.  GRPO samples a group of

@@ -27,9 +27,12 @@ TIDE_OP_EXTEND = 2
 TIDE_OP_DECODE = 3
 TIDE_OP_FULL_PREFILL = 4
 
+# bytes of the static device scratch of tide_decode_attn_noalloc (TIDE_NOALLOC_SCRATCH_BYTES)
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
 EXPORTED = ("tide_workspace_size", "tide_kv_append", "tide_extend_attn", "tide_decode_attn",
             "tide_full_prefill_attn", "tide_decode_attn_shared", "tide_workspace_size_shared",
-            "tide_decode_append_attn",
+            "tide_decode_append_attn", "tide_decode_attn_noalloc",
             "tide_ctb_create", "tide_ctb_step", "tide_ctb_get_stats", "tide_ctb_destroy",
             "tide_status_string", "tide_shutdown")
 
@@ -76,6 +79,8 @@ def load(path: str = LIB_PATH):
                                            sz, vp]
     lib.tide_decode_append_attn.argtypes = [vp, vp, vp, vp, vp, i64, vp, i32, i32, vp, dims_p,
                                             i32, vp, vp, vp, sz, vp]
+    lib.tide_decode_attn_noalloc.argtypes = [vp, vp, vp, i64, vp, i32, i32, vp, dims_p, i32, vp,
+                                             vp, vp]
     lib.tide_decode_attn_shared.argtypes = [vp, vp, vp, i64, vp, i32, i32, vp, i32, vp, vp, dims_p,
                                             i32, vp, vp, vp, sz, vp]
     lib.tide_workspace_size_shared.argtypes = [i32, vp, i32, vp, vp, dims_p, i32,
@@ -298,6 +303,22 @@ def tide_decode_append_attn(q, k_new, v_new, k_pool, v_pool, block_table, kv_len
         kv_p, ctypes.byref(dims), int(num_splits), _dev(out, torch.bfloat16, "out"),
         _dev(lse, torch.float32, "lse", nullable=True), ws, ws_n, _stream(stream)),
         "tide_decode_append_attn")
+
+
+def tide_decode_attn_noalloc(q, k_pool, v_pool, block_table, kv_lens, dims: tide_dims, out,
+                             lse=None, num_splits: int = 0, stream=None) -> None:
+    """tide_decode_attn without a workspace: runs in the library's static device scratch
+    (NOALLOC_SCRATCH_BYTES per GPU); calls that overlap on one GPU race."""
+    num_pages = _pool_shape(k_pool, v_pool, dims)
+    kv, kv_p = _host(kv_lens, "kv_lens")
+    _decode_checks(q, out, lse, block_table, kv, dims, k_pool, v_pool)
+    _check(load().tide_decode_attn_noalloc(
+        _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"),
+        _dev(v_pool, torch.bfloat16, "v_pool"), num_pages,
+        _dev(block_table, torch.int32, "block_table"), int(block_table.shape[1]), int(kv.size),
+        kv_p, ctypes.byref(dims), int(num_splits), _dev(out, torch.bfloat16, "out"),
+        _dev(lse, torch.float32, "lse", nullable=True), _stream(stream)),
+        "tide_decode_attn_noalloc")
 
 
 def _groups(group_start, shared_lens):

@@ -52,6 +52,29 @@ struct DeviceStaging {
 std::mutex g_mutex;
 std::vector<DeviceStaging*> g_staging;  // indexed by device ordinal
 
+// Device scratch of tide_decode_attn_noalloc: the work list and split partials of one
+// call, for callers that cannot allocate.  In host code `scratch` names a host-side
+// stand-in, never the device array: the device address is taken once per device with
+// hipGetSymbolAddress (with that device current) and only that address is used.
+static __device__ __align__(256) uint8_t scratch[TIDE_NOALLOC_SCRATCH_BYTES];
+
+std::mutex g_scratch_mutex;
+std::vector<void*> g_scratch_ptr;  // device address of `scratch`, indexed by device ordinal
+
+int scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return TIDE_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if ((int)g_scratch_ptr.size() <= dev) g_scratch_ptr.resize(dev + 1, nullptr);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return TIDE_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return TIDE_OK;
+}
+
 bool debug_checks() {
   const char* e = getenv("TIDE_DEBUG_CHECKS");
   return e && e[0] == '1';
@@ -164,6 +187,69 @@ int run_extend(int op, const void* q, const void* k_pool, const void* v_pool, in
   return finish(launch_extend(a, dims->head_dim, plan.waves, s), workspace, s);
 }
 
+// Shared path of tide_decode_attn, tide_decode_append_attn (fused: k_new / v_new) and
+// tide_decode_attn_noalloc (in_scratch: the call runs in the static device scratch, its
+// work list is copied there with hipMemcpyAsync from the plan's host buffer, and nothing
+// is allocated).
+int run_decode(const void* q, const void* k_new, const void* v_new, const void* k_pool,
+               const void* v_pool, int64_t num_pages, const int32_t* block_table,
+               int32_t bt_stride, int32_t num_tasks, const int32_t* kv_lens,
+               const tide_dims* dims, int32_t num_splits, void* out, float* lse,
+               void* workspace, size_t workspace_bytes, bool fused, bool in_scratch,
+               void* stream) {
+  int rc = check_dims(dims);
+  if (rc != TIDE_OK) return rc;
+  if (num_tasks < 0 || num_splits < 0) return TIDE_ERR_INVALID_ARG;
+  if (num_tasks == 0) return TIDE_OK;
+  if (num_pages <= 0 || bt_stride <= 0) return TIDE_ERR_INVALID_ARG;
+  Plan plan;
+  rc = make_plan(TIDE_OP_DECODE, num_tasks, kv_lens, nullptr, *dims, num_splits, bt_stride, true,
+                 &plan);
+  if (rc != TIDE_OK) return rc;
+  if (!q || !k_pool || !v_pool || !block_table || !out) return TIDE_ERR_INVALID_ARG;
+  if (fused && (!k_new || !v_new)) return TIDE_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (in_scratch) {
+    if (plan.total_bytes > (size_t)TIDE_NOALLOC_SCRATCH_BYTES) return TIDE_ERR_CAPACITY;
+    rc = scratch_address(&workspace);
+    if (rc != TIDE_OK) return rc;
+    // the blob starts with the zeroed header, so this also clears the error flags
+    if (hipMemcpyAsync(workspace, plan.blob.data(), plan.blob.size(), hipMemcpyHostToDevice, s) !=
+        hipSuccess)
+      return TIDE_ERR_HIP;
+  } else {
+    if (!workspace) return TIDE_ERR_INVALID_ARG;
+    if (workspace_bytes < plan.total_bytes) return TIDE_ERR_CAPACITY;
+    rc = upload(plan, workspace, s);
+    if (rc != TIDE_OK) return rc;
+  }
+  DecodeArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.block_table = block_table;
+  a.num_pages = num_pages;
+  a.bt_stride = bt_stride;
+  a.num_q_heads = dims->num_q_heads;
+  a.num_kv_heads = dims->num_kv_heads;
+  a.group = dims->num_q_heads / dims->num_kv_heads;
+  a.scale_log2 = dims->sm_scale * 1.44269504088896340736f;
+  a.num_tasks = num_tasks;
+  a.num_items = plan.num_items;
+  a.chunk = plan.chunk;
+  a.max_splits = plan.max_splits;
+  a.tasks = at<TaskDesc>(workspace, plan.tasks_off);
+  a.items = at<DecodeItem>(workspace, plan.items_off);
+  a.part_o = at_mut<float>(workspace, plan.part_o_off);
+  a.part_ml = at_mut<float>(workspace, plan.part_ml_off);
+  a.out = static_cast<uint16_t*>(out);
+  a.lse = lse;
+  a.error_flags = at_mut<int32_t>(workspace, 0);
+  a.k_new = static_cast<const uint16_t*>(k_new);
+  a.v_new = static_cast<const uint16_t*>(v_new);
+  return finish(launch_decode(a, dims->head_dim, false, s), workspace, s);
+}
+
 }  // namespace
 }  // namespace tide
 
@@ -264,46 +350,9 @@ TIDE_API int tide_decode_attn(const void* q, const void* k_pool, const void* v_p
                               int32_t num_splits, void* out, float* lse, void* workspace,
                               size_t workspace_bytes, void* stream) {
   try {
-    int rc = check_dims(dims);
-    if (rc != TIDE_OK) return rc;
-    if (num_tasks < 0 || num_splits < 0) return TIDE_ERR_INVALID_ARG;
-    if (num_tasks == 0) return TIDE_OK;
-    if (num_pages <= 0 || bt_stride <= 0) return TIDE_ERR_INVALID_ARG;
-    Plan plan;
-    rc = make_plan(TIDE_OP_DECODE, num_tasks, kv_lens, nullptr, *dims, num_splits, bt_stride,
-                   true, &plan);
-    if (rc != TIDE_OK) return rc;
-    if (!q || !k_pool || !v_pool || !block_table || !out || !workspace)
-      return TIDE_ERR_INVALID_ARG;
-    if (workspace_bytes < plan.total_bytes) return TIDE_ERR_CAPACITY;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    rc = upload(plan, workspace, s);
-    if (rc != TIDE_OK) return rc;
-    DecodeArgs a;
-    a.q = static_cast<const uint16_t*>(q);
-    a.k_pool = static_cast<const uint16_t*>(k_pool);
-    a.v_pool = static_cast<const uint16_t*>(v_pool);
-    a.block_table = block_table;
-    a.num_pages = num_pages;
-    a.bt_stride = bt_stride;
-    a.num_q_heads = dims->num_q_heads;
-    a.num_kv_heads = dims->num_kv_heads;
-    a.group = dims->num_q_heads / dims->num_kv_heads;
-    a.scale_log2 = dims->sm_scale * 1.44269504088896340736f;
-    a.num_tasks = num_tasks;
-    a.num_items = plan.num_items;
-    a.chunk = plan.chunk;
-    a.max_splits = plan.max_splits;
-    a.tasks = at<TaskDesc>(workspace, plan.tasks_off);
-    a.items = at<DecodeItem>(workspace, plan.items_off);
-    a.part_o = at_mut<float>(workspace, plan.part_o_off);
-    a.part_ml = at_mut<float>(workspace, plan.part_ml_off);
-    a.out = static_cast<uint16_t*>(out);
-    a.lse = lse;
-    a.error_flags = at_mut<int32_t>(workspace, 0);
-    a.k_new = nullptr;
-    a.v_new = nullptr;
-    return finish(launch_decode(a, dims->head_dim, false, s), workspace, s);
+    return run_decode(q, nullptr, nullptr, k_pool, v_pool, num_pages, block_table, bt_stride,
+                      num_tasks, kv_lens, dims, num_splits, out, lse, workspace, workspace_bytes,
+                      false, false, stream);
   } catch (...) {
     return TIDE_ERR_HIP;
   }
@@ -317,46 +366,23 @@ TIDE_API int tide_decode_append_attn(const void* q, const void* k_new, const voi
                                      float* lse, void* workspace, size_t workspace_bytes,
                                      void* stream) {
   try {
-    int rc = check_dims(dims);
-    if (rc != TIDE_OK) return rc;
-    if (num_tasks < 0 || num_splits < 0) return TIDE_ERR_INVALID_ARG;
-    if (num_tasks == 0) return TIDE_OK;
-    if (num_pages <= 0 || bt_stride <= 0) return TIDE_ERR_INVALID_ARG;
-    Plan plan;
-    rc = make_plan(TIDE_OP_DECODE, num_tasks, kv_lens, nullptr, *dims, num_splits, bt_stride,
-                   true, &plan);
-    if (rc != TIDE_OK) return rc;
-    if (!q || !k_new || !v_new || !k_pool || !v_pool || !block_table || !out || !workspace)
-      return TIDE_ERR_INVALID_ARG;
-    if (workspace_bytes < plan.total_bytes) return TIDE_ERR_CAPACITY;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    rc = upload(plan, workspace, s);
-    if (rc != TIDE_OK) return rc;
-    DecodeArgs a;
-    a.q = static_cast<const uint16_t*>(q);
-    a.k_pool = static_cast<const uint16_t*>(k_pool);
-    a.v_pool = static_cast<const uint16_t*>(v_pool);
-    a.block_table = block_table;
-    a.num_pages = num_pages;
-    a.bt_stride = bt_stride;
-    a.num_q_heads = dims->num_q_heads;
-    a.num_kv_heads = dims->num_kv_heads;
-    a.group = dims->num_q_heads / dims->num_kv_heads;
-    a.scale_log2 = dims->sm_scale * 1.44269504088896340736f;
-    a.num_tasks = num_tasks;
-    a.num_items = plan.num_items;
-    a.chunk = plan.chunk;
-    a.max_splits = plan.max_splits;
-    a.tasks = at<TaskDesc>(workspace, plan.tasks_off);
-    a.items = at<DecodeItem>(workspace, plan.items_off);
-    a.part_o = at_mut<float>(workspace, plan.part_o_off);
-    a.part_ml = at_mut<float>(workspace, plan.part_ml_off);
-    a.out = static_cast<uint16_t*>(out);
-    a.lse = lse;
-    a.error_flags = at_mut<int32_t>(workspace, 0);
-    a.k_new = static_cast<const uint16_t*>(k_new);
-    a.v_new = static_cast<const uint16_t*>(v_new);
-    return finish(launch_decode(a, dims->head_dim, false, s), workspace, s);
+    return run_decode(q, k_new, v_new, k_pool, v_pool, num_pages, block_table, bt_stride,
+                      num_tasks, kv_lens, dims, num_splits, out, lse, workspace, workspace_bytes,
+                      true, false, stream);
+  } catch (...) {
+    return TIDE_ERR_HIP;
+  }
+}
+
+TIDE_API int tide_decode_attn_noalloc(const void* q, const void* k_pool, const void* v_pool,
+                                      int64_t num_pages, const int32_t* block_table,
+                                      int32_t bt_stride, int32_t num_tasks,
+                                      const int32_t* kv_lens, const tide_dims* dims,
+                                      int32_t num_splits, void* out, float* lse, void* stream) {
+  try {
+    return run_decode(q, nullptr, nullptr, k_pool, v_pool, num_pages, block_table, bt_stride,
+                      num_tasks, kv_lens, dims, num_splits, out, lse, nullptr, 0, false, true,
+                      stream);
   } catch (...) {
     return TIDE_ERR_HIP;
   }

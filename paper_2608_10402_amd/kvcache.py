@@ -84,6 +84,13 @@ class PagedKV:
                                      kv_lens, self.dims, out, lse, num_splits, ws, stream)
         return out
 
+    def decode_noalloc(self, q, kv_lens, num_splits: int = 0, out=None, lse=None, stream=None):
+        """Decode in the library's static device scratch: no workspace is allocated."""
+        out = torch.empty_like(q) if out is None else out
+        _lib.tide_decode_attn_noalloc(q, self.k_pool, self.v_pool, self.block_table, kv_lens,
+                                      self.dims, out, lse, num_splits, stream)
+        return out
+
     def decode_shared(self, q, kv_lens, group_start, shared_lens, num_splits: int = 0, out=None,
                       lse=None, stream=None):
         out = torch.empty_like(q) if out is None else out

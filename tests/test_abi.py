@@ -252,6 +252,36 @@ def test_shared_decode_rejects_before_gpu():
     assert rc == tide.TIDE_OK  # no tasks: nothing to do
 
 
+# ---- decode without allocation ---------------------------------------------------------------
+def test_noalloc_decode_validation_without_gpu():
+    """tide_decode_attn_noalloc rejects bad arguments, and plans larger than its static
+    scratch, before any device work."""
+    lib = tide.load()
+    f = lib.tide_decode_attn_noalloc
+    d = ctypes.byref(GOOD)
+    one = np.array([1], np.int32)
+    bad = np.array([0], np.int32)
+    # (q, k_pool, v_pool, num_pages, bt, bt_stride, n, kv_lens, dims, splits, out, lse, stream)
+    assert f(1, 1, 1, 10, 1, 4, 1, bad.ctypes.data, d, 0, 1, None, None) == tide.TIDE_ERR_INVALID_ARG
+    assert f(1, 1, 1, 10, 1, 4, 0, None, d, 0, 1, None, None) == tide.TIDE_OK
+    assert f(None, 1, 1, 10, 1, 4, 1, one.ctypes.data, d, 0, 1, None, None) == tide.TIDE_ERR_INVALID_ARG
+    assert f(1, 1, 1, 10, 1, 4, 1, one.ctypes.data, d, -1, 1, None, None) == tide.TIDE_ERR_INVALID_ARG
+    assert f(1, 1, 1, 10, 1, 4, 1, np.array([65], np.int32).ctypes.data, d, 0, 1, None,
+             None) == tide.TIDE_ERR_CAPACITY                                # 5 pages > 4
+    # a plan whose partials exceed the static scratch
+    big = np.full(4096, 32768, np.int32)
+    rc, need = _ws(tide.TIDE_OP_DECODE, big, None, GOOD, splits=64)
+    assert rc == tide.TIDE_OK and need > _lib.NOALLOC_SCRATCH_BYTES
+    assert f(1, 1, 1, 10, 1, 2048, 4096, big.ctypes.data, d, 64, 1, None,
+             None) == tide.TIDE_ERR_CAPACITY
+
+
+def test_noalloc_scratch_size_matches_header():
+    text = open(HEADERS[0]).read()
+    m = re.search(r"#define TIDE_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == _lib.NOALLOC_SCRATCH_BYTES
+
+
 # ---- binding: shapes are checked before the C call --------------------------------------------
 def test_binding_checks_row_counts_before_the_call():
     """The C ABI takes no buffer sizes, so the binding checks every tensor against the host
@@ -284,6 +314,8 @@ def test_binding_checks_row_counts_before_the_call():
         tide.tide_decode_attn(qd[:1], kp, vp, bt, [6, 10], dims, qd)
     with pytest.raises(ValueError, match="k_new must have shape"):
         tide.tide_decode_append_attn(qd, kn, kn[:2], kp, vp, bt, [6, 10], dims, qd)
+    with pytest.raises(ValueError, match="out must have shape"):
+        tide.tide_decode_attn_noalloc(qd, kp, vp, bt, [6, 10], dims, qd[:, :4])
     with pytest.raises(ValueError, match="block_table has 2 rows"):
         tide.tide_decode_attn_shared(torch.zeros(3, 8, 64, dtype=torch.bfloat16), kp, vp, bt,
                                      [6, 10, 7], [0, 3], [0], dims,
