@@ -33,11 +33,9 @@
  * Memory layout (all device buffers are owned by the caller):
  *   element type     bf16 (raw 16-bit brain-float bit patterns) for Q, K, V, O;
  *                    fp32 for LSE.
- *   k_pool           bf16 [num_pages][num_kv_heads][page_size][head_dim]
- *                    (one (page, kv-head) block is page_size rows of head_dim contiguous)
- *   v_pool           bf16 [num_pages][num_kv_heads][head_dim][page_size]
- *                    (V is stored transposed inside each page: for one head-dim index the
- *                    page_size token slots are contiguous)
+ *   k_pool, v_pool   bf16 [num_pages][num_kv_heads][page_size][head_dim] each
+ *                    (one (page, kv-head) block is page_size token rows of head_dim
+ *                    contiguous values; the kernels transpose V operands in LDS)
  *   block_table      int32 [num_tasks][bt_stride], row-major, device memory.  Entry i of
  *                    row b is the physical page holding logical positions
  *                    [i*page_size, (i+1)*page_size) of task b.  Only the first
@@ -136,7 +134,7 @@ TIDE_API int tide_workspace_size(int op, int32_t num_tasks, const int32_t* lens_
  * For task b, new token j (0 <= j < extend_lens[b]) sits at position
  * pos = prefix_lens[b] + j and row r = indptr_b + j of k_new/v_new; for every KV head g:
  *     k_pool[BT[b][pos/16]][g][pos%16][:] = k_new[r][g][:]
- *     v_pool[BT[b][pos/16]][g][:][pos%16] = v_new[r][g][:]
+ *     v_pool[BT[b][pos/16]][g][pos%16][:] = v_new[r][g][:]
  * The copy is bit-exact; no other pool byte is written.  Two tasks must not map the
  * same (page, slot); if they do, the result for that slot is unspecified.
  */

@@ -14,7 +14,7 @@ Functions:
   prefill        full causal attention over seq_lens (== extend with P = 0)
 
 Pool layout (the library's documented one, restated independently in oracle.c):
-  K [num_pages][Hkv][16][d], V [num_pages][Hkv][d][16], bf16 bits as uint16.
+  K and V [num_pages][Hkv][16][d], bf16 bits as uint16.
 """
 from __future__ import annotations
 
@@ -76,7 +76,7 @@ def _c(a, dtype):
 
 def new_pools(num_pages: int, num_kv_heads: int, head_dim: int):
     k = np.full((num_pages, num_kv_heads, PAGE, head_dim), CANARY, dtype=np.uint16)
-    v = np.full((num_pages, num_kv_heads, head_dim, PAGE), CANARY, dtype=np.uint16)
+    v = np.full((num_pages, num_kv_heads, PAGE, head_dim), CANARY, dtype=np.uint16)
     return k, v
 
 

@@ -20,8 +20,7 @@
  *
  * Storage follows the library's documented pool layout, reimplemented here from
  * that description:
- *   K pool  [num_pages][Hkv][16][d]  (token slots, then head-dim contiguous)
- *   V pool  [num_pages][Hkv][d][16]  (head-dim, then token slots contiguous)
+ *   K pool and V pool  [num_pages][Hkv][16][d]  (token slots, then head-dim contiguous)
  *   position p of task b lives in page block_table[b][p / 16], slot p % 16.
  * Values are bf16 bit patterns; every one converts to fp64 exactly.
  */
@@ -39,14 +38,10 @@ static double bf16_bits_to_double(uint16_t h) {
   return (double)f;
 }
 
-static size_t k_slot_index(int64_t page, int g, int slot, int i, int hkv, int d) {
+/* Element i of the row at (page, kv head g, slot) in either pool. */
+static size_t slot_index(int64_t page, int g, int slot, int i, int hkv, int d) {
   return (((size_t)page * (size_t)hkv + (size_t)g) * ORACLE_PAGE + (size_t)slot) * (size_t)d +
          (size_t)i;
-}
-
-static size_t v_slot_index(int64_t page, int g, int slot, int i, int hkv, int d) {
-  return (((size_t)page * (size_t)hkv + (size_t)g) * (size_t)d + (size_t)i) * ORACLE_PAGE +
-         (size_t)slot;
 }
 
 /* Physical page of logical position p of task b, or -1 if the table does not map it. */
@@ -77,8 +72,8 @@ int oracle_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_p
       for (int g = 0; g < hkv; ++g) {
         for (int i = 0; i < d; ++i) {
           size_t src = ((size_t)row * (size_t)hkv + (size_t)g) * (size_t)d + (size_t)i;
-          k_pool[k_slot_index(page, g, slot, i, hkv, d)] = k_new[src];
-          v_pool[v_slot_index(page, g, slot, i, hkv, d)] = v_new[src];
+          k_pool[slot_index(page, g, slot, i, hkv, d)] = k_new[src];
+          v_pool[slot_index(page, g, slot, i, hkv, d)] = v_new[src];
         }
       }
     }
@@ -140,7 +135,7 @@ int oracle_attention(const uint16_t* q_sel, int64_t n_sel, const int64_t* sel_ro
       int slot = (int)(p % ORACLE_PAGE);
       double dot = 0.0;
       for (int i = 0; i < d; ++i)
-        dot += q[i] * bf16_bits_to_double(k_pool[k_slot_index(page, g, slot, i, hkv, d)]);
+        dot += q[i] * bf16_bits_to_double(k_pool[slot_index(page, g, slot, i, hkv, d)]);
       s[p] = scale * dot;
     }
     if (bad) {
@@ -167,7 +162,7 @@ int oracle_attention(const uint16_t* q_sel, int64_t n_sel, const int64_t* sel_ro
       int64_t page = page_of(bt, bt_stride, num_pages, b, p);
       int slot = (int)(p % ORACLE_PAGE);
       for (int i = 0; i < d; ++i)
-        o[i] += s[p] * bf16_bits_to_double(v_pool[v_slot_index(page, g, slot, i, hkv, d)]);
+        o[i] += s[p] * bf16_bits_to_double(v_pool[slot_index(page, g, slot, i, hkv, d)]);
     }
     for (int i = 0; i < d; ++i) o[i] /= z;
     lse[(size_t)sel * (size_t)hq + (size_t)h] = m + log(z);

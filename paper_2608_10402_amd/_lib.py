@@ -197,8 +197,8 @@ def _pool_shape(k_pool, v_pool, dims):
     n, hkv, ps, d = k_pool.shape
     if (hkv, ps, d) != (dims.num_kv_heads, dims.page_size, dims.head_dim):
         raise ValueError("k_pool must be [num_pages][Hkv][page_size][d]")
-    if tuple(v_pool.shape) != (n, hkv, d, ps):
-        raise ValueError("v_pool must be [num_pages][Hkv][d][page_size]")
+    if tuple(v_pool.shape) != (n, hkv, ps, d):
+        raise ValueError("v_pool must be [num_pages][Hkv][page_size][d]")
     return int(n)
 
 

@@ -14,17 +14,18 @@
 //     16 MFMA columns, so the prefix is read once per group of trajectories instead of
 //     once per trajectory.  Each trajectory's own keys are ordinary chunks; all of them are
 //     splits of the same merge.
-//   * K pages go through LDS, V^T pages straight into MFMA registers.  The S^T = K.Q^T
-//     operand needs 16 key rows x 16 bytes per instruction, so loading it directly reads
-//     16 half cache lines per instruction; HBM streams such a pattern about 14% slower
-//     than whole lines.  Instead each wave copies its K pages into its own LDS region
-//     with direct-to-LDS buffer loads in whole 128-byte lines (8 rows x 128 bytes per
-//     instruction) and reads the operand with ds_read_b128 from an XOR-swizzled layout
-//     that keeps the 16 rows of one read in distinct banks.  For O^T += V^T.P^T a lane
-//     loads two 8-byte pieces of transposed V pages (4 consecutive token slots of one
-//     head-dim entry in each page); one instruction covers 512 contiguous bytes.  The S^T
-//     rows of page t are its token slots, so each lane's probabilities are exactly those
-//     slots and P never moves between lanes.
+//   * K and V pages are both loaded in whole 128-byte lines.  The S^T = K.Q^T operand
+//     needs 16 key rows x 16 bytes per instruction, so loading it directly would read 16
+//     half cache lines per instruction; HBM streams such a pattern about 14% slower than
+//     whole lines.  Instead each wave copies its K pages into its own LDS region with
+//     direct-to-LDS buffer loads (8 rows x 128 bytes per instruction) and reads the
+//     operand with ds_read_b128 from an XOR-swizzled layout that keeps the 16 rows of one
+//     read in distinct banks.  V pages ([16 slots][d], like K) are loaded into registers,
+//     1 KB of contiguous rows per instruction; once the step's scores are computed, the
+//     wave writes them over its K copy in LDS and reads the O^T += V^T.P^T operands back
+//     with ds_read_b64_tr_b16, which transposes 4 key rows x 16 head-dim entries across
+//     each 16-lane group.  The S^T rows of page t are its token slots, so each lane's
+//     probabilities are exactly those slots and P never moves between lanes.
 //   * Every load instruction reads one page: the page block is a scalar base, lanes add
 //     a fixed offset.  Page ids come from scalar loads.
 //   * Two buffers in ping-pong (LDS for K, registers for V) keep the next 32-key step in
@@ -48,15 +49,32 @@ constexpr int kBigWaves = 8, kSmallWaves = 4;
 constexpr int kBigLaunchItems = 2048;  // 256 CUs x 8 waves
 constexpr int kMergeWaves = 4;
 
-// V^T operands of one 32-key step (pages p0 = keys k..k+15 and p1 = k+16..k+31):
-//   v[t][h]: head-dim tile t, slots 4*grp..4*grp+3 of page h.
+// V of one 32-key step (pages p0 = keys k..k+15 and p1 = k+16..k+31): v[h][i] is this
+// lane's 16 bytes of load i of page h, which covers page bytes 1024 i .. 1024 i + 1023.
 // The step's K pages sit in a per-wave LDS buffer.
 template <int D>
 struct DecodeRegs {
-  uint2 v[D / 16][2];
+  static constexpr int kLoads = kPage * D * 2 / 1024;  // 1 KB loads per page
+  u32x4 v[2][kLoads];
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// V page layout in LDS, written over the step's K copy once its scores are computed: row
+// r (16 of them, 2D bytes each) keeps its order, and its 32-byte blocks are XOR-swizzled
+// by vsw(r), so that the 8 rows x 32 bytes a half-wave reads with ds_read_b64_tr_b16 fall
+// in distinct banks, and the 16 lanes of a 16-byte write of one row too.
+template <int D>
+struct VLds {
+  static constexpr int kNG = D / 8;  // 16-byte granules per row
+  static __device__ __forceinline__ int vsw(int r) { return D == 128 ? (r & 7) : ((r >> 1) & 3); }
+  // byte offset, inside a page copy, of 16-byte granule g of row r
+  static __device__ __forceinline__ uint32_t offset(int r, int g) {
+    return (uint32_t)(r * 2 * D + 32 * ((g >> 1) ^ vsw(r)) + 16 * (g & 1));
+  }
+};
 
 // K page layout in LDS.  A page block is 16 key rows of D bf16 (2D bytes = D/8 granules
 // of 16 bytes).  It is copied by 2 * (D/64) direct-to-LDS instructions; instruction
@@ -100,7 +118,7 @@ constexpr int kStreamPolicy = 2;
 constexpr int kSharedPolicy = 0;
 
 // Loads of one step.  Every instruction reads a single page block: the K pages go to
-// kbuf (page t at t * kPageBytes), the V^T pieces to registers.
+// kbuf (page t at t * kPageBytes), the V rows to registers.
 template <int D, int kPolicy>
 __device__ __forceinline__ void load_step(DecodeRegs<D>& r, uint8_t* kbuf,
                                           __amdgpu_buffer_rsrc_t k0, __amdgpu_buffer_rsrc_t k1,
@@ -116,12 +134,18 @@ __device__ __forceinline__ void load_step(DecodeRegs<D>& r, uint8_t* kbuf,
                                              16, k_src[i], 0, 0, kPolicy);
   }
 #pragma unroll
-  for (int t = 0; t < D / 16; ++t) {
-    r.v[t][0] = __builtin_bit_cast(
-        uint2, __builtin_amdgcn_raw_buffer_load_b64(v0, v_off + 512 * t, 0, kPolicy));
-    r.v[t][1] = __builtin_bit_cast(
-        uint2, __builtin_amdgcn_raw_buffer_load_b64(v1, v_off + 512 * t, 0, kPolicy));
+  for (int i = 0; i < DecodeRegs<D>::kLoads; ++i) {
+    r.v[0][i] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(v0, v_off + 1024 * i, 0, kPolicy));
+    r.v[1][i] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(v1, v_off + 1024 * i, 0, kPolicy));
   }
+}
+
+// Transposed read of 4 key rows x 16 head-dim entries of a V page (ds_read_b64_tr_b16).
+__device__ __forceinline__ uint2 read_tr(const uint8_t* p) {
+  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+  return __builtin_bit_cast(uint2, v);
 }
 
 // Keep only the first n (0..4) bf16 elements of an 8-byte V^T piece.
@@ -200,7 +224,22 @@ void decode_split_kernel(DecodeArgs a) {
   // S^T operand c of a page: row `col`, granule 4c + grp; granules 4c + grp for even and
   // odd c differ only in bit 2 and in g / 8 = c / 2, which adds 1 KB
   const uint32_t k_rd_even = L::lds_offset(col, grp), k_rd_odd = L::lds_offset(col, 4 + grp);
-  const uint32_t v_off = (uint32_t)(col * kPage * 2 + 8 * grp);    // head-dim row `col`
+  const uint32_t v_off = (uint32_t)(16 * lane);  // this lane's 16 bytes of each 1 KB V load
+  // LDS byte offsets: where this lane's V granules go (load i of a page covers rows
+  // i * rpl + lane / kNG), and the transposed operand reads of head-dim tile t: rows
+  // 4 grp + gl / 4, entries 16t + 4 (gl % 4) .. + 3 for lane gl of 16-lane group grp,
+  // so lane l receives V[4 grp + e][16t + l % 16] in slot e.
+  using VL = VLds<D>;
+  constexpr int kRpl = 1024 / (2 * D);  // rows per 1 KB load
+  uint32_t v_wr[DecodeRegs<D>::kLoads];
+#pragma unroll
+  for (int i = 0; i < DecodeRegs<D>::kLoads; ++i)
+    v_wr[i] = VL::offset(i * kRpl + lane / VL::kNG, lane % VL::kNG);
+  const int gl = lane & 15, vr = 4 * grp + (gl >> 2);
+  uint32_t v_rd[D / 16];
+#pragma unroll
+  for (int t = 0; t < D / 16; ++t)
+    v_rd[t] = (uint32_t)(vr * 2 * D + 32 * (t ^ VL::vsw(vr)) + 8 * (gl & 3));
 
   // Page ids come from scalar loads, so that no wait for one ever waits for the K/V
   // loads in flight.  A page past the context (or with an invalid id) gets a buffer
@@ -263,13 +302,6 @@ void decode_split_kernel(DecodeArgs a) {
         s[t][e] = x;
         mt = fmaxf(mt, x);
       }
-    if (tail) {  // V slots past kend must not reach the MFMA (NaN * 0 = NaN)
-#pragma unroll
-      for (int t = 0; t < D / 16; ++t)
-#pragma unroll
-        for (int hp = 0; hp < 2; ++hp)
-          cur.v[t][hp] = keep_first4(cur.v[t][hp], kend - (k + 16 * hp + 4 * grp));
-    }
     mt = fmaxf(mt, xor_shfl(mt, 16));
     mt = fmaxf(mt, xor_shfl(mt, 32));
     if (__any(mt > m_ref + kRescaleSlack)) {
@@ -294,16 +326,30 @@ void decode_split_kernel(DecodeArgs a) {
         l_exact += p0 + p1;
       }
     const bf16x8 pb = as_bf16x8(w);
+    // V over the K copy (its reads are done: the MFMAs above consumed them), then the
+    // transposed operands back; LDS keeps one wave's accesses in order
+    uint8_t* vbuf = const_cast<uint8_t*>(kbuf);
+#pragma unroll
+    for (int hp = 0; hp < 2; ++hp)
+#pragma unroll
+      for (int i = 0; i < DecodeRegs<D>::kLoads; ++i)
+        *reinterpret_cast<u32x4*>(vbuf + hp * L::kPageBytes + v_wr[i]) = cur.v[hp][i];
 #pragma unroll
     for (int t = 0; t < D / 16; ++t) {
-      const u32x4 vv = {cur.v[t][0].x, cur.v[t][0].y, cur.v[t][1].x, cur.v[t][1].y};
+      uint2 v0 = read_tr(vbuf + v_rd[t]);
+      uint2 v1 = read_tr(vbuf + L::kPageBytes + v_rd[t]);
+      if (tail) {  // V slots past kend must not reach the MFMA (NaN * 0 = NaN)
+        v0 = keep_first4(v0, kend - (k + 4 * grp));
+        v1 = keep_first4(v1, kend - (k + 16 + 4 * grp));
+      }
+      const u32x4 vv = {v0.x, v0.y, v1.x, v1.y};
       o[t] = mfma16(as_bf16x8(vv), pb, o[t]);
     }
   };
 
   if constexpr (kAppend) {
-    // The split that ends the context appends its newest token before reading: K row
-    // and V^T column of slot pos % 16.  Its loads of earlier steps overlap the stores;
+    // The split that ends the context appends its newest token before reading: the K
+    // and V rows of slot pos % 16.  Its loads of earlier steps overlap the stores;
     // the step that holds the slot waits for them (in `load`), so its loads return the
     // new token.  No other wave reads this page (splits end on 32-key boundaries, other
     // kv heads' blocks are whole 4 KB pages, and pages past a context are never read),
@@ -316,12 +362,13 @@ void decode_split_kernel(DecodeArgs a) {
         const int64_t row = (int64_t)td.row_start * a.num_kv_heads + kv_h;
         const int64_t blk = ((int64_t)p * a.num_kv_heads + kv_h) * (int64_t)(kPage * D);
         uint16_t* kdst = const_cast<uint16_t*>(a.k_pool) + blk + (int64_t)slot * D;
-        uint16_t* vdst = const_cast<uint16_t*>(a.v_pool) + blk + slot;
+        uint16_t* vdst = const_cast<uint16_t*>(a.v_pool) + blk + (int64_t)slot * D;
         const uint16_t* kn = a.k_new + row * D;
         const uint16_t* vn = a.v_new + row * D;
-        if (lane < D / 8) store_u32x4(kdst + 8 * lane, load_u32x4(kn + 8 * lane));
-#pragma unroll
-        for (int d = lane; d < D; d += 64) vdst[d * kPage] = vn[d];
+        if (lane < D / 8) {
+          store_u32x4(kdst + 8 * lane, load_u32x4(kn + 8 * lane));
+          store_u32x4(vdst + 8 * lane, load_u32x4(vn + 8 * lane));
+        }
       } else {
         flag_error = true;
       }

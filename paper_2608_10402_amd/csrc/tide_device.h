@@ -198,9 +198,9 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
 // Row permutation for the 32x32 tiles.  When the 32 rows of an S^T = K.Q^T tile are the
 // keys kappa(0..31), the D registers r = 0..7 of lane l hold keys 8*(l/32) + r and
 // registers 8..15 hold 16 + 8*(l/32) + (r - 8): each lane owns runs of 8 consecutive
-// keys, which is exactly the B operand of the P.V product over 16 keys.  The same
-// permutation applied to the rows of V^T makes each lane's outputs 8 consecutive
-// head-dim entries, so results leave in 16-byte stores.
+// keys, which is exactly the B operand of the P.V product over 16 keys.  The V^T operand
+// of that product is read so that its rows follow the same pattern over the head-dim
+// entries, which makes each lane's outputs 8 consecutive entries (16-byte stores).
 __device__ __forceinline__ int perm32(int rho) {
   const int j = rho >> 3, h = (rho >> 2) & 1, r = rho & 3;
   return 16 * (j >> 1) + 8 * h + 4 * (j & 1) + r;

@@ -22,8 +22,7 @@ class PagedKV:
         self.device = torch.device(device)
         self.dims = _lib.make_dims(num_q_heads, num_kv_heads, head_dim,
                                    sm_scale if sm_scale is not None else 1.0 / math.sqrt(head_dim))
-        shape_k = (num_pages, num_kv_heads, 16, head_dim)
-        shape_v = (num_pages, num_kv_heads, head_dim, 16)
+        shape_k = shape_v = (num_pages, num_kv_heads, 16, head_dim)
         if fill_canary:
             self.k_pool = torch.full(shape_k, CANARY_BITS, dtype=torch.int16,
                                      device=self.device).view(torch.bfloat16)

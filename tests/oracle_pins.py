@@ -266,9 +266,9 @@ def pin_append(wl: W.Workload, lib=None):
             page = int(wl.block_table[b, pos // 16])
             slot = pos % 16
             assert np.array_equal(kp[page, :, slot, :], kn[row]), (b, j)
-            assert np.array_equal(vp[page, :, :, slot], vn[row]), (b, j)
+            assert np.array_equal(vp[page, :, slot, :], vn[row]), (b, j)
             touched_k[page, :, slot, :] = True
-            touched_v[page, :, :, slot] = True
+            touched_v[page, :, slot, :] = True
             row += 1
     assert (kp[~touched_k] == oracle.CANARY).all()
     assert (vp[~touched_v] == oracle.CANARY).all()

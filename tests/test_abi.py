@@ -290,7 +290,7 @@ def test_binding_checks_row_counts_before_the_call():
     import torch
     dims = _lib.make_dims(8, 2, 64, 0.125)
     kp = torch.zeros(10, 2, 16, 64, dtype=torch.bfloat16)
-    vp = torch.zeros(10, 2, 64, 16, dtype=torch.bfloat16)
+    vp = torch.zeros(10, 2, 16, 64, dtype=torch.bfloat16)
     bt = torch.zeros(2, 4, dtype=torch.int32)
     q = torch.zeros(7, 8, 64, dtype=torch.bfloat16)    # 3 + 4 rows
     with pytest.raises(ValueError, match="q must have shape"):

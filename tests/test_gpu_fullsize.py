@@ -53,13 +53,12 @@ def _check_append_pages(wl, dw, tasks, upto_fn):
         n = upto_fn(b)
         pages = torch.as_tensor(wl.block_table[b, : -(-n // 16)].astype(np.int64), device=kp.device)
         gk = host_bits(kp[pages])  # [npages, Hkv, 16, d]
-        gv = host_bits(vp[pages])  # [npages, Hkv, d, 16]
+        gv = host_bits(vp[pages])  # [npages, Hkv, 16, d]
         k = wl.k_rows(b, 0, n)
         v = wl.v_rows(b, 0, n)
         pos = np.arange(n)
         assert np.array_equal(gk[pos // 16, :, pos % 16, :], k), "task %d K pages" % b
-        assert np.array_equal(np.transpose(gv, (0, 3, 1, 2))[pos // 16, pos % 16], v), \
-            "task %d V pages" % b
+        assert np.array_equal(gv[pos // 16, :, pos % 16, :], v), "task %d V pages" % b
 
 
 @pytest.fixture(scope="module")
@@ -195,7 +194,7 @@ def _check_stale_pages(wl, dw, tasks):
         pages = torch.as_tensor(wl.block_table[b, pos // 16].astype(np.int64), device=kp.device)
         slots = torch.as_tensor(pos % 16, device=kp.device)
         gk = host_bits(kp[pages, :, slots, :])  # [n, Hkv, d]
-        gv = host_bits(vp[pages, :, :, slots])  # [n, Hkv, d]
+        gv = host_bits(vp[pages, :, slots, :])  # [n, Hkv, d]
         assert np.array_equal(gk, wl.stale_rows("k", b, n, s)), "task %d stale K" % b
         assert np.array_equal(gv, wl.stale_rows("v", b, n, s)), "task %d stale V" % b
 

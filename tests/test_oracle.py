@@ -84,16 +84,21 @@ MUTANTS = {
     "causal_off_by_one": ("int64_t t = (int64_t)prefix_lens[b] + (row - indptr[b]);",
                           "int64_t t = (int64_t)prefix_lens[b] + (row - indptr[b]) + 1;"),
     "gqa_modulo_map": ("int g = h / group;", "int g = h % hkv;"),
-    "v_read_with_k_layout": ("v_pool[v_slot_index(page, g, slot, i, hkv, d)]);",
-                             "v_pool[k_slot_index(page, g, slot, i, hkv, d)]);"),
+    "v_read_from_k_pool": ("s[p] * bf16_bits_to_double(v_pool[", "s[p] * bf16_bits_to_double(k_pool["),
+    "v_read_transposed": (
+        "bf16_bits_to_double(v_pool[slot_index(page, g, slot, i, hkv, d)]);",
+        "bf16_bits_to_double(v_pool[(((size_t)page * (size_t)hkv + (size_t)g) * (size_t)d + "
+        "(size_t)i) * ORACLE_PAGE + (size_t)slot]);"),
     "softmax_sign": ("s[p] = exp(s[p] - m);", "s[p] = exp(m - s[p]);"),
     "lse_without_max": ("= m + log(z);", "= log(z);"),
     "unnormalized_output": ("o[i] /= z;", "o[i] /= 1.0;"),
     "slot_index_shift": ("int slot = (int)(p % ORACLE_PAGE);\n      double dot",
                          "int slot = (int)((p + 1) % ORACLE_PAGE);\n      double dot"),
     "append_row_index": ("size_t src = ((size_t)row *", "size_t src = ((size_t)j *"),
-    "append_v_transposed": ("v_pool[v_slot_index(page, g, slot, i, hkv, d)] = v_new[src];",
-                            "v_pool[k_slot_index(page, g, slot, i, hkv, d)] = v_new[src];"),
+    "append_v_transposed": (
+        "v_pool[slot_index(page, g, slot, i, hkv, d)] = v_new[src];",
+        "v_pool[(((size_t)page * (size_t)hkv + (size_t)g) * (size_t)d + (size_t)i) * ORACLE_PAGE + "
+        "(size_t)slot] = v_new[src];"),
 }
 
 
