@@ -67,12 +67,13 @@ PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
 # rocprofv3 counter summaries (copy-calibrated FETCH_SIZE + WRITE_SIZE per launch), keyed by
 # (workload, dominant kernel); each records the hash of the kernel source it was taken on.
 PROFILE_SUMMARIES = {
-    ("agent_resume_7b", "extend"): ("attn_extend_agent_resume_7b_counters.txt", "attn_extend.hip"),
-    ("resumed_decode", "decode"): ("decode_split_resumed_decode_counters.txt", "attn_decode.hip"),
-    ("grpo_group_decode", "shared_decode"): ("decode_split_grpo_group_decode_counters.txt",
-                                             "attn_decode.hip"),
-    ("multimodal_prune_resume", "extend"): ("attn_extend_multimodal_prune_resume_counters.txt",
-                                            "attn_extend.hip"),
+    ("agent_resume_7b", "extend"): "attn_extend_agent_resume_7b_counters.txt",
+    ("resumed_decode", "decode"): "decode_split_resumed_decode_counters.txt",
+    ("grpo_group_decode", "shared_decode"): "decode_split_grpo_group_decode_counters.txt",
+    ("multimodal_prune_resume", "extend"): "attn_extend_multimodal_prune_resume_counters.txt",
+    ("multimodal_resume", "extend"): "attn_extend_multimodal_resume_counters.txt",
+    ("long_horizon", "extend"): "attn_extend_long_horizon_counters.txt",
+    ("long_horizon", "decode"): "decode_split_long_horizon_counters.txt",
 }
 
 
@@ -132,14 +133,28 @@ def append_bytes(wl, tokens: int) -> float:
     return float(tokens) * s.num_kv_heads * s.head_dim * 2 * 2 * 2  # K+V, read + write
 
 
+def source_digest() -> str:
+    """sha256 over every kernel and host source in csrc/ (names and bytes, sorted by name)
+    and the build script that holds the compiler flags: a counter summary is only valid for
+    the exact build it was taken from."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_10402_amd", "csrc")
+    files = sorted(os.listdir(csrc)) + ["../build.py"]
+    for name in files:
+        path = os.path.join(csrc, name)
+        if os.path.isfile(path):
+            h.update(os.path.basename(name).encode() + b"\0")
+            h.update(open(path, "rb").read())
+    return h.hexdigest()
+
+
 def counter_traffic(workload: str, kernel: str):
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter
-    summary, or None when there is none or the kernel source changed since."""
+    summary, or None when there is none or any source or build flag changed since."""
     entry = PROFILE_SUMMARIES.get((workload, kernel))
     if entry is None:
         return None
-    path = os.path.join(ROOT, "profiles", entry[0])
-    src = os.path.join(ROOT, "paper_2608_10402_amd", "csrc", entry[1])
+    path = os.path.join(ROOT, "profiles", entry)
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -147,56 +162,126 @@ def counter_traffic(workload: str, kernel: str):
     m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not m_hash or not m_bytes:
         return None
-    cur = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    return float(m_bytes.group(1)) if cur == m_hash.group(1) else None
+    return float(m_bytes.group(1)) if source_digest() == m_hash.group(1) else None
 
 
-def cpu_baseline(wl, q_ext_host, budget_s: float):
-    """The fp64 oracle on a bounded, seeded sample of extend rows (host cores)."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _task_pool(wl, b: int, n_pos: int):
+    """The oracle's pool image of task b alone (positions 0 .. n_pos - 1 in pages 0, 1, ..),
+    built by the oracle's own append from the seeded generator."""
     import oracle
     s = wl.spec
-    kp, vp = oracle.new_pools(wl.num_pages, s.num_kv_heads, s.head_dim)
-    zeros = np.zeros(wl.num_tasks, np.int32)
-    oracle.kv_append(wl.packed("k", wl.prefix_ranges()), wl.packed("v", wl.prefix_ranges()),
-                     kp, vp, wl.block_table, zeros, wl.prefix_lens)
-    oracle.kv_append(wl.packed("k", wl.extend_ranges()), wl.packed("v", wl.extend_ranges()),
-                     kp, vp, wl.block_table, wl.prefix_lens, wl.extend_lens)
-    indptr = np.concatenate([[0], np.cumsum(wl.extend_lens)]).astype(np.int64)
-    rng = np.random.default_rng(2608)
-    rows = []
-    for b in range(wl.num_tasks):
-        e = int(wl.extend_lens[b])
-        if e:
-            rows += [indptr[b], indptr[b] + e - 1]
-    rows += rng.integers(0, int(indptr[-1]), size=4096).tolist()
-    rows = np.array(list(dict.fromkeys(int(r) for r in rows)), dtype=np.int64)
-    rng.shuffle(rows)
+    n_pages = max(1, -(-n_pos // 16))
+    kp, vp = oracle.new_pools(n_pages, s.num_kv_heads, s.head_dim)
+    bt = np.arange(n_pages, dtype=np.int32).reshape(1, -1)
+    oracle.kv_append(wl.k_rows(b, 0, n_pos), wl.v_rows(b, 0, n_pos), kp, vp, bt,
+                     np.array([0], np.int32), np.array([n_pos], np.int32))
+    return kp, vp, bt
+
+
+def _oracle_rows(wl, b: int, positions, n_pos: int, threads: int):
+    """fp64 oracle for query positions of task b (each attends keys 0 .. its position);
+    returns (out [n, Hq, d], seconds spent in the oracle itself)."""
+    import oracle
+    s = wl.spec
+    kp, vp, bt = _task_pool(wl, b, n_pos)
+    pos = np.asarray(positions, np.int64)
+    q = np.concatenate([wl.q_rows(b, int(t), int(t) + 1) for t in pos])
+    t0 = time.perf_counter()
+    o, _ = oracle.attention(q, pos, kp, vp, bt, np.array([0], np.int32),
+                            np.array([n_pos], np.int32), s.num_q_heads, wl.sm_scale,
+                            nthreads=threads)
+    return o, time.perf_counter() - t0
+
+
+def cpu_baseline_extend(wl, budget_s: float, extra_rows: int = 46):
+    """The fp64 oracle on a bounded sample of extend rows, timed on the host cores: every
+    task's first and last new row plus `extra_rows` seeded ones, all query heads.  Only the
+    oracle's own calls are timed (building each task's pool image is not)."""
+    import oracle
+    s = wl.spec
     threads = oracle.threads()
-    done, flops, t0 = 0, 0.0, time.time()
-    outs = []
-    while done < rows.size and time.time() - t0 < budget_s:
-        batch = rows[done:done + 4 * threads]
-        o, _ = oracle.attention(q_ext_host[batch], batch, kp, vp, wl.block_table, wl.prefix_lens,
-                                wl.extend_lens, s.num_q_heads, wl.sm_scale, nthreads=threads)
-        task = np.searchsorted(indptr, batch, side="right") - 1
-        pos = wl.prefix_lens[task] + (batch - indptr[task])
-        flops += 4.0 * s.head_dim * s.num_q_heads * float(np.sum(pos + 1))
-        outs.append((batch, o))
-        done += batch.size
-    dt = time.time() - t0
-    info = {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": "%d of %d extend rows (every task's first and last row, then seeded "
-                      "random rows), all %d query heads, fp64, %.1f s wall"
-                      % (done, int(indptr[-1]), s.num_q_heads, dt),
-            "seconds": round(dt, 2), "flops": flops}
+    rng = np.random.default_rng(2608)
+    indptr = np.concatenate([[0], np.cumsum(wl.extend_lens)]).astype(np.int64)
+    secs, flops, rows, outs = 0.0, 0.0, 0, []
+    for b in rng.permutation(wl.num_tasks):
+        b = int(b)
+        p, e = int(wl.prefix_lens[b]), int(wl.extend_lens[b])
+        if e == 0:
+            continue
+        local = sorted(set([0, e - 1] + rng.integers(0, e, size=extra_rows).tolist()))
+        pos = [p + j for j in local]
+        o, dt = _oracle_rows(wl, b, pos, p + e, threads)
+        secs += dt
+        flops += 4.0 * s.head_dim * s.num_q_heads * float(sum(t + 1 for t in pos))
+        rows += len(pos)
+        outs.append((np.array([indptr[b] + j for j in local], np.int64), o))
+        if secs > budget_s:
+            break
+    full = extend_flops(wl)
+    info = {"value": flops / secs / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(),
+            "sample": "%d of %d extend rows (each sampled task's first and last row plus %d "
+                      "seeded ones), all %d query heads, fp64; %.1f s of oracle time"
+                      % (rows, int(indptr[-1]), extra_rows, s.num_q_heads, secs),
+            "seconds": round(secs, 2), "flops": flops,
+            "extrapolated_full_config_s": round(secs * full / flops, 1),
+            "extrapolation": "sample time x (full-config FLOPs / sample FLOPs); not measured"}
     return info, outs
 
 
-class Stage:
-    """One timed call of the step: a callable plus its algorithmic work."""
+def cpu_baseline_decode(wl, budget_s: float, steps: int = 1):
+    """The fp64 oracle over the decode queries of every task (steps consecutive decode
+    positions per task), timed on the host cores; GB/s over the same algorithmic bytes as
+    the GPU figure.  Only the oracle's own calls are timed."""
+    import oracle
+    s = wl.spec
+    threads = oracle.threads()
+    secs, nbytes, tasks = 0.0, 0.0, 0
+    for b in range(wl.num_tasks):
+        L = int(wl.seq_lens[b])
+        if steps == 1:  # the decoded token is the last of the context
+            pos, n_pos = [L - 1], L
+        else:           # decode steps after the resume: positions L .. L + steps - 1
+            pos, n_pos = [L + i for i in range(steps)], L + steps
+        _, dt = _oracle_rows(wl, b, pos, n_pos, threads)
+        secs += dt
+        kv = np.array([t + 1 for t in pos])
+        nbytes += float(kv.sum()) * s.num_kv_heads * s.head_dim * 4 + \
+            len(pos) * s.num_q_heads * s.head_dim * 4 + float((-(-kv // 16)).sum()) * 4
+        tasks += 1
+        if secs > budget_s:
+            break
+    info = {"value": nbytes / secs / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(),
+            "sample": "%s: %d of %d tasks x %d decode step(s), all %d query heads, fp64; "
+                      "%.1f s of oracle time" % ("full coverage" if tasks == wl.num_tasks else
+                                                 "sample", tasks, wl.num_tasks, steps,
+                                                 s.num_q_heads, secs),
+            "seconds": round(secs, 2), "bytes": nbytes}
+    if tasks < wl.num_tasks:
+        info["extrapolated_full_config_s"] = round(secs * wl.num_tasks / tasks, 1)
+        info["extrapolation"] = "sample time x (all tasks / sampled tasks); not measured"
+    return info
 
-    def __init__(self, name, fn, flops=0.0, bytes_=0.0):
+
+class Stage:
+    """One timed call of the step: a callable plus its algorithmic work.  in_step=False
+    marks a comparison (the same work done another way), timed on its own but not part of
+    the step."""
+
+    def __init__(self, name, fn, flops=0.0, bytes_=0.0, in_step=True):
         self.name, self.fn, self.flops, self.bytes = name, fn, flops, bytes_
+        self.in_step = in_step
         self.times = []
 
 
@@ -216,6 +301,13 @@ def build_stages(wl, kv, dev, args, torch, np_up):
                             bytes_=append_bytes(wl, int(wl.extend_lens.sum()))))
         stages.append(Stage("extend", lambda: kv.extend(q_ext, wl.prefix_lens, wl.extend_lens, out=out_ext),
                             flops=extend_flops(wl)))
+        # the same resume with the append fused into the attention (tide_extend_append_attn)
+        out_fused = torch.empty_like(q_ext)
+        keep.update(out_fused_ext=out_fused)
+        stages.append(Stage("fused_append_extend",
+                            lambda: kv.extend_append(q_ext, k_ext, v_ext, wl.prefix_lens,
+                                                     wl.extend_lens, out=out_fused),
+                            flops=extend_flops(wl), in_step=False))
     if s.kind in ("extend", "prune_resume"):
         last = np.cumsum(wl.extend_lens) - 1
         q_dec = keep["q_ext"][torch.from_numpy(last.astype(np.int64)).to(dev)].contiguous()
@@ -257,17 +349,17 @@ def build_stages(wl, kv, dev, args, torch, np_up):
                             bytes_=decode_bytes(wl, wl.seq_lens) + append_bytes(wl, wl.num_tasks)))
         keep.update(out_dec=out_dec, out_fused=out_fused)
     if s.kind == "long_horizon":
+        # eight generated tokens per task, each appended and attended in one fused call
+        # (tide_decode_append_attn); the bytes are the decode's plus the token's append
         for step in range(s.decode_steps):
             rng = wl.decode_ranges(step)
             pos = (wl.seq_lens + step).astype(np.int32)
             kn, vn, qn = (np_up(wl.packed(x, rng)) for x in ("k", "v", "q"))
             on = torch.empty_like(qn)
-            stages.append(Stage("append_decode_%d" % step,
-                                (lambda kn=kn, vn=vn, pos=pos: kv.append(kn, vn, pos, ones)),
-                                bytes_=append_bytes(wl, wl.num_tasks)))
             stages.append(Stage("decode_%d" % step,
-                                (lambda qn=qn, on=on, pos=pos: kv.decode(qn, pos + 1, out=on)),
-                                bytes_=decode_bytes(wl, pos + 1)))
+                                (lambda qn=qn, kn=kn, vn=vn, on=on, pos=pos:
+                                 kv.decode_append(qn, kn, vn, pos + 1, out=on)),
+                                bytes_=decode_bytes(wl, pos + 1) + append_bytes(wl, wl.num_tasks)))
     return stages, keep
 
 
@@ -510,8 +602,10 @@ def main():
     setup_s = time.time() - t_setup
     stream = torch.cuda.current_stream()
 
+    step_stages = [st for st in stages if st.in_step]
+
     def step():
-        for st in stages:
+        for st in step_stages:
             st.fn()
 
     for _ in range(args.warmup):
@@ -531,7 +625,24 @@ def main():
     # event pair (its work-list upload, its kernels and launch gaps included).  Timing
     # events placed between different stages inside a step attribute the time around a
     # kernel boundary imprecisely, so they are not used for the per-stage figures.
+    # A stage that moves less than 1 GB could be served from the 256 MB MALL and the L2s
+    # when repeated back to back, so it is timed call by call, with 512 MB of scratch
+    # overwritten between calls (outside the events).
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     for st in stages:
+        if st.flops == 0 and st.bytes < 1e9:
+            evs = []
+            for r in range(args.steps):
+                flush.fill_(r & 0xFF)
+                ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                ea.record(stream)
+                st.fn()
+                eb.record(stream)
+                evs.append((ea, eb))
+            torch.cuda.synchronize()
+            st.times.append(sum(a_.elapsed_time(b_) for a_, b_ in evs) / args.steps)
+            st.flushed = True
+            continue
         ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         ea.record(stream)
         for _ in range(args.steps):
@@ -539,6 +650,7 @@ def main():
         eb.record(stream)
         torch.cuda.synchronize()
         st.times.append(ea.elapsed_time(eb) / args.steps)
+    del flush
     ms = {st.name: float(np.mean(st.times)) for st in stages}
 
     def total(prefix):
@@ -547,10 +659,17 @@ def main():
                 sum(st.bytes for st in sel))
 
     extra = {"stage_ms": {k: round(v, 4) for k, v in ms.items()}, "setup_s": round(setup_s, 1),
-             "wall_ms_per_step": round(wall * 1e3 / args.steps, 3)}
+             "wall_ms_per_step": round(wall * 1e3 / args.steps, 3),
+             "stages_timed_per_call_with_cache_flush": [st.name for st in stages
+                                                        if getattr(st, "flushed", False)]}
     rooflines = {}
+    if "fused_append_extend" in ms:
+        extra["speedup_fused_vs_append_then_extend"] = round(
+            (ms["append_new"] + ms["extend"]) / ms["fused_append_extend"], 3)
+        extra["fused_extend_vs_separate_bitwise_equal"] = bool(torch.equal(
+            keep["out_ext"].view(torch.int16), keep["out_fused_ext"].view(torch.int16)))
     if "extend" in ms:
-        t, f, _ = total("extend")
+        t, f = ms["extend"], extend_flops(wl)
         v = f / (t * 1e-3) / 1e12
         rooflines["extend"] = {"bound": "mfma", "achieved": round(v, 2), "peak": PEAK_BF16_TFLOPS,
                                "unit": "TFLOP/s", "frac": round(v / PEAK_BF16_TFLOPS, 4)}
@@ -618,7 +737,7 @@ def main():
 
     cpu = None
     if args.cpu_seconds > 0 and "extend" in ms:
-        cpu, outs = cpu_baseline(wl, wl.packed("q", wl.extend_ranges()), args.cpu_seconds)
+        cpu, outs = cpu_baseline_extend(wl, args.cpu_seconds)
         got = keep["out_ext"].float().cpu().numpy()
         errs = [np.abs(got[b] - o) for b, o in outs]
         if errs:
@@ -626,6 +745,11 @@ def main():
             extra["parity_sampled_rows"] = {"rows": int(sum(len(b) for b, _ in outs)),
                                             "max_abs_err": float(e.max()),
                                             "mean_abs_err": float(e.mean())}
+        if s.decode_steps:
+            extra["cpu_baseline_decode"] = cpu_baseline_decode(wl, args.cpu_seconds,
+                                                               steps=s.decode_steps)
+    elif args.cpu_seconds > 0 and ("decode" in ms or "shared_decode" in ms):
+        cpu = cpu_baseline_decode(wl, args.cpu_seconds)
 
     line = {
         "metric": METRIC,

@@ -16,10 +16,11 @@
  *     tide_extend_attn        attention of the new tokens over retained prefix + themselves
  *     tide_decode_attn        one query token per task over its whole context (split-K)
  *     tide_full_prefill_attn  causal attention over the whole sequence (the recompute path)
- *   and two variants of decode: for GRPO groups whose trajectories share a prompt prefix,
- *   and with the append of the decoded token fused in:
- *     tide_decode_attn_shared tide_decode_attn, reading each shared prefix once per group
+ *   the same steps with the KV-append fused into the attention:
+ *     tide_extend_append_attn tide_kv_append of the new tokens + tide_extend_attn
  *     tide_decode_append_attn tide_kv_append of one token per task + tide_decode_attn
+ *   and decode for GRPO groups whose trajectories share a prompt prefix:
+ *     tide_decode_attn_shared tide_decode_attn, reading each shared prefix once per group
  *
  *   The attention itself is standard scaled dot-product attention (Vaswani et al.,
  *   2017), which the paper uses but does not restate: for a query row at absolute
@@ -162,6 +163,26 @@ TIDE_API int tide_extend_attn(const void* q, const void* k_pool, const void* v_p
                      const int32_t* prefix_lens, const int32_t* extend_lens,
                      const tide_dims* dims, void* out, float* lse, void* workspace,
                      size_t workspace_bytes, void* stream);
+
+/*
+ * Extend attention with the KV-append of the new tokens fused in: the result and the pool
+ * contents afterwards are those of tide_kv_append(k_new, v_new, prefix_lens, extend_lens)
+ * followed by tide_extend_attn(q, prefix_lens, extend_lens).  Every resume with a retained
+ * cache (Section 4.2) appends its new observation/action tokens and then attends over
+ * them; fusing removes the append launch and the pool round trip of the new rows.
+ *   k_new, v_new  bf16 [rows][Hkv][d], packed by extend_lens like q: the new tokens' K/V.
+ * The attention reads keys at or past each task's prefix straight from k_new / v_new, and
+ * each (task, kv head, block of new tokens) work item writes its own tokens' rows into
+ * their pool slots; no work item of the call reads those slots, so there is no ordering
+ * between them.  Workspace: tide_workspace_size(TIDE_OP_EXTEND, ...).  Arguments and errors
+ * as tide_extend_attn, plus TIDE_ERR_INVALID_ARG for a NULL k_new / v_new.
+ */
+TIDE_API int tide_extend_append_attn(const void* q, const void* k_new, const void* v_new,
+                            void* k_pool, void* v_pool, int64_t num_pages,
+                            const int32_t* block_table, int32_t bt_stride, int32_t num_tasks,
+                            const int32_t* prefix_lens, const int32_t* extend_lens,
+                            const tide_dims* dims, void* out, float* lse, void* workspace,
+                            size_t workspace_bytes, void* stream);
 
 /*
  * Decode attention: one query token per task (the action tokens generated between

@@ -11,7 +11,7 @@ from ._lib import (TIDE_ERR_CAPACITY, TIDE_ERR_HIP, TIDE_ERR_INVALID_ARG, TIDE_E
                    TIDE_ERR_UNSUPPORTED, TIDE_OK, TIDE_OP_DECODE, TIDE_OP_EXTEND,
                    TIDE_OP_FULL_PREFILL, TIDE_OP_KV_APPEND, TideError, alloc_workspace, load,
                    make_dims, status_string, tide_decode_append_attn, tide_decode_attn,
-                   tide_decode_attn_noalloc, NOALLOC_SCRATCH_BYTES,
+                   tide_decode_attn_noalloc, NOALLOC_SCRATCH_BYTES, tide_extend_append_attn,
                    tide_decode_attn_shared, tide_dims,
                    tide_extend_attn, tide_full_prefill_attn, tide_kv_append, tide_shutdown,
                    tide_workspace_size, tide_workspace_size_shared)
@@ -23,5 +23,5 @@ __all__ = ["TIDE_ERR_CAPACITY", "TIDE_ERR_HIP", "TIDE_ERR_INVALID_ARG", "TIDE_ER
            "make_dims", "status_string", "tide_decode_attn", "tide_dims", "tide_extend_attn",
            "tide_full_prefill_attn", "tide_kv_append", "tide_shutdown", "tide_workspace_size",
            "tide_decode_attn_shared", "tide_workspace_size_shared", "tide_decode_append_attn",
-           "tide_decode_attn_noalloc", "NOALLOC_SCRATCH_BYTES",
+           "tide_decode_attn_noalloc", "NOALLOC_SCRATCH_BYTES", "tide_extend_append_attn",
            "PagedKV"]

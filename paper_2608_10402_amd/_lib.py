@@ -32,7 +32,7 @@ NOALLOC_SCRATCH_BYTES = 64 << 20
 
 EXPORTED = ("tide_workspace_size", "tide_kv_append", "tide_extend_attn", "tide_decode_attn",
             "tide_full_prefill_attn", "tide_decode_attn_shared", "tide_workspace_size_shared",
-            "tide_decode_append_attn", "tide_decode_attn_noalloc",
+            "tide_decode_append_attn", "tide_decode_attn_noalloc", "tide_extend_append_attn",
             "tide_ctb_create", "tide_ctb_step", "tide_ctb_get_stats", "tide_ctb_destroy",
             "tide_status_string", "tide_shutdown")
 
@@ -79,6 +79,8 @@ def load(path: str = LIB_PATH):
                                            sz, vp]
     lib.tide_decode_append_attn.argtypes = [vp, vp, vp, vp, vp, i64, vp, i32, i32, vp, dims_p,
                                             i32, vp, vp, vp, sz, vp]
+    lib.tide_extend_append_attn.argtypes = [vp, vp, vp, vp, vp, i64, vp, i32, i32, vp, vp, dims_p,
+                                            vp, vp, vp, sz, vp]
     lib.tide_decode_attn_noalloc.argtypes = [vp, vp, vp, i64, vp, i32, i32, vp, dims_p, i32, vp,
                                              vp, vp]
     lib.tide_decode_attn_shared.argtypes = [vp, vp, vp, i64, vp, i32, i32, vp, i32, vp, vp, dims_p,
@@ -269,6 +271,33 @@ def _decode_checks(q, out, lse, block_table, kv, dims, *others):
     _lse(lse, n, dims.num_q_heads)
     _block_table(block_table, n)
     _same_device(q, out, lse, block_table, *others)
+
+
+def tide_extend_append_attn(q, k_new, v_new, k_pool, v_pool, block_table, prefix_lens,
+                            extend_lens, dims: tide_dims, out, lse=None, workspace=None,
+                            stream=None) -> None:
+    num_pages = _pool_shape(k_pool, v_pool, dims)
+    p, p_p = _host(prefix_lens, "prefix_lens")
+    e, e_p = _host(extend_lens, "extend_lens")
+    if p is None or e is None or p.size != e.size:
+        raise ValueError("prefix_lens and extend_lens must have one entry per task")
+    rows = _lens_total(e)
+    _rows(q, "q", rows, dims.num_q_heads, dims.head_dim)
+    _rows(out, "out", rows, dims.num_q_heads, dims.head_dim)
+    _rows(k_new, "k_new", rows, dims.num_kv_heads, dims.head_dim)
+    _rows(v_new, "v_new", rows, dims.num_kv_heads, dims.head_dim)
+    _lse(lse, rows, dims.num_q_heads)
+    _block_table(block_table, int(p.size))
+    _same_device(q, k_new, v_new, k_pool, v_pool, block_table, out, lse, workspace)
+    ws, ws_n = _ws(workspace)
+    _check(load().tide_extend_append_attn(
+        _dev(q, torch.bfloat16, "q"), _dev(k_new, torch.bfloat16, "k_new"),
+        _dev(v_new, torch.bfloat16, "v_new"), _dev(k_pool, torch.bfloat16, "k_pool"),
+        _dev(v_pool, torch.bfloat16, "v_pool"), num_pages,
+        _dev(block_table, torch.int32, "block_table"), int(block_table.shape[1]), int(p.size),
+        p_p, e_p, ctypes.byref(dims), _dev(out, torch.bfloat16, "out"),
+        _dev(lse, torch.float32, "lse", nullable=True), ws, ws_n, _stream(stream)),
+        "tide_extend_append_attn")
 
 
 def tide_decode_attn(q, k_pool, v_pool, block_table, kv_lens, dims: tide_dims, out, lse=None,

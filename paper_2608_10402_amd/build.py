@@ -20,7 +20,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB_PATH = os.path.join(PKG, "libtide.so")
 
-HIP_SOURCES = ["tide_api.hip", "attn_extend.hip", "attn_decode.hip", "kv_append.hip"]
+HIP_SOURCES = ["tide_api.hip", "attn_extend.hip", "attn_extend_append.hip", "attn_decode.hip",
+               "kv_append.hip"]
 CXX_SOURCES = ["plan.cpp", "ctb.cpp"]
 ARCH = "gfx950"
 

@@ -144,10 +144,13 @@ T* at_mut(void* ws, size_t off) {
 }
 
 // Shared path of tide_extend_attn and tide_full_prefill_attn.
+// With k_new / v_new (tide_extend_append_attn) the new tokens' K/V are appended by the
+// attention kernel itself.
 int run_extend(int op, const void* q, const void* k_pool, const void* v_pool, int64_t num_pages,
                const int32_t* block_table, int32_t bt_stride, int32_t num_tasks,
                const int32_t* lens_a, const int32_t* lens_b, const tide_dims* dims, void* out,
-               float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+               float* lse, void* workspace, size_t workspace_bytes, void* stream,
+               const void* k_new = nullptr, const void* v_new = nullptr, bool fused = false) {
   int rc = check_dims(dims);
   if (rc != TIDE_OK) return rc;
   if (num_tasks < 0) return TIDE_ERR_INVALID_ARG;
@@ -158,11 +161,14 @@ int run_extend(int op, const void* q, const void* k_pool, const void* v_pool, in
   if (rc != TIDE_OK) return rc;
   if (plan.num_items == 0) return TIDE_OK;
   if (!q || !k_pool || !v_pool || !block_table || !out || !workspace) return TIDE_ERR_INVALID_ARG;
+  if (fused && (!k_new || !v_new)) return TIDE_ERR_INVALID_ARG;
   if (workspace_bytes < plan.total_bytes) return TIDE_ERR_CAPACITY;
   hipStream_t s = static_cast<hipStream_t>(stream);
   rc = upload(plan, workspace, s);
   if (rc != TIDE_OK) return rc;
   ExtendArgs a;
+  a.k_new = fused ? static_cast<const uint16_t*>(k_new) : nullptr;
+  a.v_new = fused ? static_cast<const uint16_t*>(v_new) : nullptr;
   a.q = static_cast<const uint16_t*>(q);
   a.k_pool = static_cast<const uint16_t*>(k_pool);
   a.v_pool = static_cast<const uint16_t*>(v_pool);
@@ -325,6 +331,22 @@ TIDE_API int tide_extend_attn(const void* q, const void* k_pool, const void* v_p
     return run_extend(TIDE_OP_EXTEND, q, k_pool, v_pool, num_pages, block_table, bt_stride,
                       num_tasks, prefix_lens, extend_lens, dims, out, lse, workspace,
                       workspace_bytes, stream);
+  } catch (...) {
+    return TIDE_ERR_HIP;
+  }
+}
+
+TIDE_API int tide_extend_append_attn(const void* q, const void* k_new, const void* v_new,
+                                     void* k_pool, void* v_pool, int64_t num_pages,
+                                     const int32_t* block_table, int32_t bt_stride,
+                                     int32_t num_tasks, const int32_t* prefix_lens,
+                                     const int32_t* extend_lens, const tide_dims* dims, void* out,
+                                     float* lse, void* workspace, size_t workspace_bytes,
+                                     void* stream) {
+  try {
+    return run_extend(TIDE_OP_EXTEND, q, k_pool, v_pool, num_pages, block_table, bt_stride,
+                      num_tasks, prefix_lens, extend_lens, dims, out, lse, workspace,
+                      workspace_bytes, stream, k_new, v_new, true);
   } catch (...) {
     return TIDE_ERR_HIP;
   }

@@ -136,6 +136,11 @@ struct ExtendArgs {
   float* part_o;
   float* part_ml;
   int32_t total_rows;
+  // fused append (non-null k_new): the new tokens' K/V rows, packed like q by extend_lens,
+  // [rows][Hkv][d].  Keys at or past a task's prefix are read from them instead of the
+  // pool, and each item writes its own tokens' rows into the pool.
+  const uint16_t* k_new;
+  const uint16_t* v_new;
 };
 
 struct DecodeArgs {

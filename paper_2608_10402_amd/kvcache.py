@@ -65,6 +65,16 @@ class PagedKV:
                               extend_lens, self.dims, out, lse, ws, stream)
         return out
 
+    def extend_append(self, q, k_new, v_new, prefix_lens, extend_lens, out=None, lse=None,
+                      stream=None):
+        """Append the new tokens' K/V and run extend attention, fused in one call."""
+        out = torch.empty_like(q) if out is None else out
+        ws = self.workspace(_lib.tide_workspace_size(_lib.TIDE_OP_EXTEND, prefix_lens,
+                                                     extend_lens, self.dims))
+        _lib.tide_extend_append_attn(q, k_new, v_new, self.k_pool, self.v_pool, self.block_table,
+                                     prefix_lens, extend_lens, self.dims, out, lse, ws, stream)
+        return out
+
     def decode(self, q, kv_lens, num_splits: int = 0, out=None, lse=None, stream=None):
         out = torch.empty_like(q) if out is None else out
         ws = self.workspace(_lib.tide_workspace_size(_lib.TIDE_OP_DECODE, kv_lens, None,
