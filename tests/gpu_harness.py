@@ -119,29 +119,33 @@ def assert_lse(gpu: torch.Tensor, ref: np.ndarray, what: str, tol=LSE_TOL):
     assert mx <= tol, "%s: lse error %.4g > %.4g" % (what, mx, tol)
 
 
-def oracle_task_rows(wl: W.Workload, b: int, rows, upto: int | None = None,
-                     q_rows: np.ndarray | None = None):
-    """fp64 oracle for selected query positions of task b, from a compact pool that holds
-    only task b (its own append, its own page order).  `rows` are absolute positions;
-    each attends to keys 0..row.  `upto` = number of positions to place (default: the
-    last requested row + 1).  Returns (sorted rows, out [n, Hq, d], lse [n, Hq])."""
+def oracle_task_pool(wl: W.Workload, b: int, n_pos: int):
+    """Oracle pool images holding task b alone (positions 0 .. n_pos - 1, its own page
+    order), written by the oracle's own append from the seeded generator."""
     s = wl.spec
-    rows = np.asarray(sorted(rows), dtype=np.int64)
-    n_pos = int(upto if upto is not None else rows.max() + 1)
     n_pages = -(-n_pos // 16)
     perm = np.random.default_rng(b + 17).permutation(n_pages).astype(np.int32)
     bt = perm.reshape(1, -1)
     kp, vp = oracle.new_pools(n_pages, s.num_kv_heads, s.head_dim)
     oracle.kv_append(wl.k_rows(b, 0, n_pos), wl.v_rows(b, 0, n_pos), kp, vp, bt,
                      np.array([0], np.int32), np.array([n_pos], np.int32))
-    outs, lses = [], []
-    for r in rows:
-        q = wl.q_rows(b, int(r), int(r) + 1) if q_rows is None else q_rows[[list(rows).index(r)]]
-        o, l = oracle.extend(q, kp, vp, bt, np.array([r], np.int32), np.array([1], np.int32),
-                             s.num_q_heads, wl.sm_scale)
-        outs.append(o[0])
-        lses.append(l[0])
-    return rows, np.stack(outs), np.stack(lses)
+    return kp, vp, bt
+
+
+def oracle_task_rows(wl: W.Workload, b: int, rows, upto: int | None = None, pool=None):
+    """fp64 oracle for selected query positions of task b, from a compact pool that holds
+    only task b (its own append, its own page order).  `rows` are absolute positions;
+    each attends to keys 0..row.  `upto` = number of positions to place (default: the
+    last requested row + 1); `pool` = (kp, vp, bt) from oracle_task_pool, reused.
+    Returns (sorted rows, out [n, Hq, d], lse [n, Hq])."""
+    s = wl.spec
+    rows = np.asarray(sorted(rows), dtype=np.int64)
+    n_pos = int(upto if upto is not None else rows.max() + 1)
+    kp, vp, bt = pool if pool is not None else oracle_task_pool(wl, b, n_pos)
+    q = np.concatenate([wl.q_rows(b, int(r), int(r) + 1) for r in rows])
+    out, lse = oracle.attention(q, rows, kp, vp, bt, np.array([0], np.int32),
+                                np.array([n_pos], np.int32), s.num_q_heads, wl.sm_scale)
+    return rows, out, lse
 
 
 def sample_tasks(wl: W.Workload, k: int, seed: int = 0):
