@@ -164,6 +164,96 @@ __device__ __forceinline__ uint2 keep_first4(uint2 x, int n) {
 // a.k_new / a.v_new into its pool slot, and waits for the stores before it issues the
 // loads of the step that holds the slot.  No other split reads that slot, so the result
 // equals appending first and then decoding.
+// Partials of plain decode travel between CUs, possibly on different XCDs, whose L2s are
+// not kept coherent for ordinary accesses.  They are therefore stored and loaded with
+// device-scope cache policy (SC1: the store writes through to the device's coherence
+// point, the load does not take a possibly stale cached line), which makes the heavy
+// cache write-back and invalidate of a device-scope fence unnecessary: a wave waits for
+// its partial stores to complete before it counts its arrival, and the merging wave
+// loads the partials only after its count returned.
+constexpr int kDeviceScope = 16;  // buffer cache policy bit SC1
+
+__device__ __forceinline__ void store_f32x4_device(float* base, uint32_t bytes, uint32_t off,
+                                                   f32x4 v) {
+  const auto rsrc = __builtin_amdgcn_make_buffer_rsrc(base, 0, bytes, 0x00020000);
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rsrc, off, 0, kDeviceScope);
+}
+
+// Merge of the n >= 2 split partials of the G query heads of one (task, kv head), by one
+// wave: lanes 8j .. 8j + 7 take head j (a second pass takes heads 8 .. 15), each lane D/8
+// consecutive head-dim entries.  With M = max_s m_s and w_s = 2^(m_s - M), the row is
+// sum_s w_s o_s / sum_s w_s l_s and its LSE ln(sum_s w_s l_exact_s) + M ln 2.  Every sum
+// runs over the splits in split order, so the result does not depend on which split
+// finished last.
+template <int D>
+__device__ __forceinline__ void merge_kv_head(const DecodeArgs& a, int task, int kv_h, int n) {
+  constexpr int kPer = D / 8;  // head-dim entries per lane
+  constexpr int kBatch = 4;    // splits whose partials are loaded together
+  const int lane = threadIdx.x & 63;
+  const int hh = lane >> 3, sub = lane & 7;
+  const int G = a.group;
+  for (int j0 = 0; j0 < G; j0 += 8) {
+    const int j = j0 + hh;
+    const bool ok = j < G;
+    const int64_t row = (int64_t)task * a.num_q_heads + kv_h * G + (ok ? j : 0);
+    const auto ml = __builtin_amdgcn_make_buffer_rsrc(a.part_ml + row * a.max_splits * 4, 0,
+                                                      a.max_splits * 16, 0x00020000);
+    const auto po = __builtin_amdgcn_make_buffer_rsrc(a.part_o + row * a.max_splits * D, 0,
+                                                      a.max_splits * D * 4, 0x00020000);
+    float mx = kNoMax;
+    for (int s0 = 0; s0 < n; s0 += 16) {
+      float m[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        m[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                             ml, 16 * min(s0 + i, n - 1), 0, kDeviceScope));
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, m[i]);  // repeats of split n-1 are harmless
+    }
+    f32x4 acc[kPer / 4];
+#pragma unroll
+    for (int k = 0; k < kPer / 4; ++k) acc[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    float l_round = 0.0f, l_ex = 0.0f;
+    for (int s0 = 0; s0 < n; s0 += kBatch) {
+      f32x4 st[kBatch], src[kBatch][kPer / 4];
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        const int sp = min(s0 + i, n - 1);  // past n: a valid slot, not summed below
+        st[i] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                              ml, 16 * sp, 0, kDeviceScope));
+#pragma unroll
+        for (int k = 0; k < kPer / 4; ++k)
+          src[i][k] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                    po, 4 * (sp * D + kPer * sub + 4 * k), 0,
+                                                    kDeviceScope));
+      }
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        if (s0 + i < n) {
+          const float w = fast_exp2(st[i][0] - mx);
+          l_round += w * st[i][1];
+          l_ex += w * st[i][2];
+#pragma unroll
+          for (int k = 0; k < kPer / 4; ++k) acc[k] += w * src[i][k];
+        }
+      }
+    }
+    if (ok) {
+      const float inv = 1.0f / l_round;
+      uint16_t* orow = a.out + row * D + kPer * sub;
+#pragma unroll
+      for (int k = 0; k < kPer / 8; ++k) {
+        const u32x4 w = {pack_bf16x2(acc[2 * k][0] * inv, acc[2 * k][1] * inv),
+                         pack_bf16x2(acc[2 * k][2] * inv, acc[2 * k][3] * inv),
+                         pack_bf16x2(acc[2 * k + 1][0] * inv, acc[2 * k + 1][1] * inv),
+                         pack_bf16x2(acc[2 * k + 1][2] * inv, acc[2 * k + 1][3] * inv)};
+        store_u32x4(orow + 8 * k, w);
+      }
+      if (a.lse && sub == 0) a.lse[row] = (mx + __log2f(l_ex)) * kLn2;
+    }
+  }
+}
+
 template <int D, bool kShared, bool kAppend, int kWaves>
 __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void decode_split_kernel(DecodeArgs a) {
@@ -417,30 +507,78 @@ void decode_split_kernel(DecodeArgs a) {
   l_tot += xor_shfl(l_tot, 32);
   float l_ex = l_exact + xor_shfl(l_exact, 16);
   l_ex += xor_shfl(l_ex, 32);
+  if constexpr (!kShared) {
+    const int nsplit = td.aux;
+    if (nsplit == 1) {
+      // the task's only split: its rows are final (the merge of one partial is this
+      // same arithmetic: weight 2^0 = 1, output o / l)
+      if (col_ok) {
+        const float inv = 1.0f / l_tot;
+        uint16_t* orow = a.out + qrow * D;
+#pragma unroll
+        for (int t = 0; t < D / 16; ++t) {
+          const uint2 w = {pack_bf16x2(o[t][0] * inv, o[t][1] * inv),
+                           pack_bf16x2(o[t][2] * inv, o[t][3] * inv)};
+          *reinterpret_cast<uint2*>(orow + 16 * t + 4 * grp) = w;
+        }
+        if (a.lse && grp == 0) a.lse[qrow] = (m_ref + __log2f(l_ex)) * kLn2;
+      }
+      return;
+    }
+  }
   if (col_ok) {
     const int64_t slot =
         ((int64_t)ctask * a.num_q_heads + kv_h * G + chead) * a.max_splits + split;
     float* po = a.part_o + slot * D;
+    const f32x4 ml = {m_ref, l_tot, l_ex, 0.0f};
+    if constexpr (kShared) {  // merged by a second kernel
 #pragma unroll
-    for (int t = 0; t < D / 16; ++t)
-      *reinterpret_cast<f32x4*>(po + 16 * t + 4 * grp) = o[t];
-    if (grp == 0) {
-      f32x4 ml = {m_ref, l_tot, l_ex, 0.0f};
-      *reinterpret_cast<f32x4*>(a.part_ml + slot * 4) = ml;
+      for (int t = 0; t < D / 16; ++t)
+        *reinterpret_cast<f32x4*>(po + 16 * t + 4 * grp) = o[t];
+      if (grp == 0) *reinterpret_cast<f32x4*>(a.part_ml + slot * 4) = ml;
+    } else if (a.tickets) {  // merged in this kernel, possibly by a wave on another XCD
+#pragma unroll
+      for (int t = 0; t < D / 16; ++t)
+        store_f32x4_device(po, D * 4, 4 * (16 * t + 4 * grp), o[t]);
+      if (grp == 0) store_f32x4_device(a.part_ml + slot * 4, 16, 0, ml);
+    } else {  // merged by the merge kernel
+#pragma unroll
+      for (int t = 0; t < D / 16; ++t)
+        *reinterpret_cast<f32x4*>(po + 16 * t + 4 * grp) = o[t];
+      if (grp == 0) *reinterpret_cast<f32x4*>(a.part_ml + slot * 4) = ml;
+    }
+  }
+  if constexpr (!kShared) {
+    if (a.tickets) {
+      // Arrival count of this (task, kv head); the split that completes it merges.  The
+      // partial stores complete before the count is taken, and the merge's loads issue
+      // only after it returned (both device-scope, see store_f32x4_device).
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      int arrived = 0;
+      if (lane == 0)
+        arrived = __hip_atomic_fetch_add(a.tickets + (int64_t)first_task * a.num_kv_heads + kv_h,
+                                         1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      arrived = __shfl(arrived, 0, 64);
+      asm volatile("" ::: "memory");
+      if (arrived != td.aux - 1) return;
+      merge_kv_head<D>(a, first_task, kv_h, td.aux);
     }
   }
 }
 
-// One wave per (task, query head): combine the task's split partials.
-template <int D>
+// One wave per (task, query head): combine the task's split partials.  kSkipSingle: a
+// task with one split already wrote its rows (plain decode).
+template <int D, bool kSkipSingle>
 __global__ __launch_bounds__(kMergeWaves * 64) void decode_merge_kernel(DecodeArgs a) {
   // wave-uniform and 32-bit (the launch has num_tasks * Hq < 2^31 waves)
   const int row = (int)blockIdx.x * kMergeWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (row >= a.num_tasks * a.num_q_heads) return;
   const int task = row / a.num_q_heads;
+  const int n = a.tasks[task].aux;
+  if (kSkipSingle && n == 1) return;
   const int64_t r = row;
   merge_partials<D>(a.part_ml + r * a.max_splits * 4, 4, a.part_o + r * a.max_splits * D, D,
-                    a.tasks[task].aux, a.out + r * D, a.lse ? a.lse + r : nullptr);
+                    n, a.out + r * D, a.lse ? a.lse + r : nullptr);
 }
 
 template <int D, bool kShared, bool kAppend>
@@ -458,12 +596,13 @@ hipError_t launch(const DecodeArgs& a, hipStream_t stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  if (!kShared && a.tickets) return hipSuccess;  // merged inside the split kernel
   const int64_t rows = (int64_t)a.num_tasks * a.num_q_heads;
   if (rows >= INT32_MAX - kMergeWaves) return hipErrorInvalidValue;
   if (rows > 0) {
     const int blocks = (int)((rows + kMergeWaves - 1) / kMergeWaves);
-    hipLaunchKernelGGL((decode_merge_kernel<D>), dim3(blocks), dim3(kMergeWaves * 64), 0,
-                       stream, a);
+    hipLaunchKernelGGL((decode_merge_kernel<D, !kShared>), dim3(blocks), dim3(kMergeWaves * 64),
+                       0, stream, a);
   }
   return hipGetLastError();
 }

@@ -41,6 +41,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 constexpr int64_t kDecodeTargetItems = 4096;
 constexpr int64_t kDecodeMinChunk = 512;
 constexpr int64_t kDecodeMaxChunk = 16384;
+constexpr int64_t kFoldMeanSplits = 4;  // merge inside the split kernel up to this mean
 
 // Per-task (prefix, extend) of the positions this call touches or attends.
 int task_lengths(int op, int32_t b, const int32_t* lens_a, const int32_t* lens_b, int32_t* prefix,
@@ -472,6 +473,11 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
     plan->chunk = (int32_t)chunk;
     plan->max_splits = max_splits;
     n_items = (int64_t)items.size();
+    // The split kernel merges a (task, kv head) in its last split when tasks have few
+    // splits on average; with many, the merge tail at the end of the launch (each merge
+    // one wave, latency-bound) costs more than a merge kernel (measured on MI355X: at 2.5
+    // splits per task the fold saves the merge kernel's 10 us; at 16 it adds 40-57 us).
+    plan->fold_merge = n_items <= (int64_t)kFoldMeanSplits * num_tasks * dims.num_kv_heads;
     if (build_blob) {
       items_bytes.resize(items.size() * sizeof(DecodeItem));
       if (!items.empty()) memcpy(items_bytes.data(), items.data(), items_bytes.size());
@@ -490,6 +496,10 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
   if (plan->split) {
     plan->merge_rows_off = off;
     off = align_up(off + (size_t)plan->total_rows * sizeof(MergeRow), kWsAlign);
+  }
+  if (op == TIDE_OP_DECODE) {  // left zero in the blob: every call starts the counts at 0
+    plan->tickets_off = off;
+    off = align_up(off + (size_t)num_tasks * dims.num_kv_heads * sizeof(int32_t), kWsAlign);
   }
   plan->upload_bytes = off;
   if (plan->split) {

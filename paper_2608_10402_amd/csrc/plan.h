@@ -24,6 +24,10 @@ struct Plan {
   // extend split-KV plan: per-row merge descriptors (uploaded after the items)
   bool split = false;
   size_t merge_rows_off = 0;
+  // decode: per-(task, kv head) arrival counters, zeros in the uploaded blob, used when
+  // the split kernel merges (fold_merge: few splits per task) instead of a merge kernel
+  size_t tickets_off = 0;
+  bool fold_merge = false;
   int64_t row_slots = 0;  // partial row slots (each holds every query head)
   // the planner's run-time estimates (microseconds) of the plain and chosen extend plans;
   // 0 when the call was too large to consider splitting

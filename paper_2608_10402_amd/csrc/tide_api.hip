@@ -253,6 +253,7 @@ int run_decode(const void* q, const void* k_new, const void* v_new, const void* 
   a.error_flags = at_mut<int32_t>(workspace, 0);
   a.k_new = static_cast<const uint16_t*>(k_new);
   a.v_new = static_cast<const uint16_t*>(v_new);
+  a.tickets = plan.fold_merge ? at_mut<int32_t>(workspace, plan.tickets_off) : nullptr;
   return finish(launch_decode(a, dims->head_dim, false, s), workspace, s);
 }
 
@@ -476,6 +477,7 @@ TIDE_API int tide_decode_attn_shared(const void* q, const void* k_pool, const vo
     a.error_flags = at_mut<int32_t>(workspace, 0);
     a.k_new = nullptr;
     a.v_new = nullptr;
+    a.tickets = nullptr;
     return finish(launch_decode(a, dims->head_dim, true, s), workspace, s);
   } catch (...) {
     return TIDE_ERR_HIP;

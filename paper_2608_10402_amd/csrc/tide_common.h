@@ -171,6 +171,10 @@ struct DecodeArgs {
   // and uses them directly.  Null for a plain decode.
   const uint16_t* k_new;
   const uint16_t* v_new;
+  // plain decode: one arrival counter per (task, kv head), zero at launch (uploaded with
+  // the work list); the split that brings it to the task's split count merges that kv
+  // head's rows.  Null for the shared-prefix variant, which merges in a second kernel.
+  int32_t* tickets;
 };
 
 }  // namespace tide

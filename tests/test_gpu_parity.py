@@ -188,3 +188,37 @@ def test_long_horizon_sequence():
     torch.cuda.synchronize()
     assert np.array_equal(host_bits(dw.kv.k_pool), kp)
     assert np.array_equal(host_bits(dw.kv.v_pool), vp)
+
+
+@pytest.mark.parametrize("splits", [0, 1, 2, 3, 40])
+def test_decode_every_row_merged_once(splits):
+    """Every decode row is written exactly by one of: the task's only split (1 split),
+    the split that finishes its (task, kv head) last (few splits per task: 2, 3), or the
+    merge kernel (many: 40, and the automatic plan at this size).  Outputs and LSE start
+    as NaN on every call, so a row nobody wrote shows; repeated calls are bit-identical
+    (merges sum in split order, whichever split arrives last) and match the oracle.  64
+    tasks of mixed lengths spread the splits of one task over many CUs and XCDs."""
+    rng = np.random.default_rng(31)
+    prefix = [int(x) for x in rng.integers(0, 5000, size=64)]
+    prefix[:4] = [0, 15, 31, 4095]
+    wl = W.custom_workload(28, 4, 128, prefix, [1] * 64, seed=11)
+    dw = DeviceWorkload(wl)
+    dw.append_extend()
+    kp, vp = oracle_pools(wl)
+    q = wl.packed("q", wl.extend_ranges())
+    ref, ref_lse = oracle.decode(q, kp, vp, wl.block_table, wl.seq_lens, wl.spec.num_q_heads,
+                                 wl.sm_scale)
+    qd = dev_bf16(q)
+    outs = []
+    for _ in range(3):
+        out = torch.full_like(qd, float("nan"))
+        lse = torch.full((q.shape[0], q.shape[1]), float("nan"), dtype=torch.float32, device="cuda")
+        dw.kv.decode(qd, wl.seq_lens, num_splits=splits, out=out, lse=lse)
+        torch.cuda.synchronize()
+        assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all()
+        outs.append((out, lse))
+    assert_close(outs[0][0], ref, "decode merged in kernel, splits=%d" % splits)
+    assert_lse(outs[0][1], ref_lse, "decode merged in kernel, splits=%d" % splits)
+    for o, l in outs[1:]:
+        assert torch.equal(o.view(torch.int16), outs[0][0].view(torch.int16))
+        assert torch.equal(l, outs[0][1])
