@@ -32,7 +32,7 @@
  *   TIDE_CTB_POLICY_CTB      Algorithm 1 as above;
  *   TIDE_CTB_POLICY_REQUEST  request-level continuous batching with prefix caching and a
  *                            fixed task concurrency (the fixed-concurrency baseline of
- *                            Section 7): each turn is a request, first-come first-served;
+ *                            Section 6.5): each turn is a request, first-come first-served;
  *                            the newest running request is preempted when pages run out,
  *                            and nothing waiting is admitted in a round that preempted.
  *

@@ -19,7 +19,7 @@ What it follows (Section 4):
     and a group's trajectories are admitted to the rank its first trajectory went to.
 
 The baseline is request-level continuous batching with prefix caching and a fixed task
-concurrency (the "F9/F10" settings of Section 7): every turn is a request; a finished
+concurrency (the "F9/F10" settings of Section 6.5): every turn is a request; a finished
 request's pages stay cached in LRU order until reused; FCFS admission; the newest running
 request is preempted when pages run out.
 
@@ -351,7 +351,7 @@ class Sim:
 
     # ---------------------------------------------------------------- request policy
     def schedule_request(self):
-        """Request-level batching.  Reading of the engine (vLLM-like, Section 7 baseline):
+        """Request-level batching.  Reading of the engine (vLLM-like, the Section 6.5 baseline):
         a fixed number of tasks in flight; a new task goes to the rank with the fewest tasks
         in flight; per rank, running requests first get the page their next token needs,
         preempting the newest running request (to the front of the queue) when pages run

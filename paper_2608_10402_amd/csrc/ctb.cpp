@@ -1,5 +1,5 @@
 // Host-side Continuous Task Batching scheduler (Section 4) and the request-level
-// baseline it is compared with (Section 7), driving the paged-KV engine model described
+// baseline it is compared with (Section 6.5), driving the paged-KV engine model described
 // in include/tide_ctb.h.
 //
 // Data structures (all per rank unless noted):

@@ -590,8 +590,8 @@ int make_plan_shared(int32_t num_tasks, const int32_t* kv_lens, int32_t num_grou
     const int32_t np = (int32_t)ceil_div(sh, chunk);
     // The items of one (kv head, chunk) -- one per run of per_item trajectories -- read the
     // same prefix keys.  They are consecutive, so they share a workgroup of the decode
-    // kernel (four waves, one item each, on one CU) or a neighbouring one, and the later
-    // reads hit that XCD's L2.
+    // kernel (four or eight waves by launch size, one item each, on one CU) or a
+    // neighbouring one, and the later reads hit that XCD's L2.
     for (int32_t h = 0; h < dims.num_kv_heads; ++h)
       for (int32_t j = 0; j < np; ++j)
         for (int32_t f = s0; f < s1; f += per_item) {

@@ -1,8 +1,9 @@
 """Out-of-range page ids (needs an MI355X).
 
 The ABI guarantees that a block-table entry outside [0, num_pages) is never dereferenced:
-every kernel reads page 0 in its place (append writes nothing for it) and sets an error
-flag in the workspace, which TIDE_DEBUG_CHECKS=1 turns into TIDE_ERR_PAGE_RANGE.  Each
+the attention kernels read it through a zero-range buffer descriptor (zeros, no memory
+access), append writes nothing for it, and each sets an error flag in the workspace,
+which TIDE_DEBUG_CHECKS=1 turns into TIDE_ERR_PAGE_RANGE.  Each
 entry point is called with one bad entry (too large, then negative) in a page it reads or
 writes -- extend under both the plain and the split-KV plan -- and must report the error;
 the same calls on the valid table must not.

@@ -6,7 +6,7 @@ groups), each trajectory a sequence of turns.  Turn k of a trajectory first appe
 that), then generates `gen_tokens[k]` tokens one at a time, then waits `env_rounds[k]`
 engine rounds for the environment (not after its last turn).  Trajectories of one group
 share the prompt length.  Shapes follow the task-statistics table of Appendix C (WebShop:
-about 8 turns and 3400 tokens per trajectory) and the single-instance step of Section 7
+about 8 turns and 3400 tokens per trajectory) and the single-instance step of Section 6.5
 (32 training groups of 8 and 200 evaluation groups of 4 trajectories).
 
 K/V/Q rows of trajectory t at position p come from the same counter-based generator as
