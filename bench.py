@@ -165,6 +165,26 @@ def counter_traffic(workload: str, kernel: str):
     return float(m_bytes.group(1)) if source_digest() == m_hash.group(1) else None
 
 
+def kernel_label(wl, stage: str) -> str:
+    """The instantiation the stage's dominant kernel runs as, from the plan the library
+    makes for these lengths (tide_plan_info_get): extend<D, lse, split, append>,
+    decode_split<D, shared, append, waves per workgroup>."""
+    import paper_2608_10402_amd as tide
+    s = wl.spec
+    dims = tide.make_dims(s.num_q_heads, s.num_kv_heads, s.head_dim, wl.sm_scale)
+    d = s.head_dim
+    if stage == "extend":
+        info = tide.tide_plan_info_get(tide.TIDE_OP_EXTEND, wl.prefix_lens, wl.extend_lens, dims)
+        return "extend_attn_kernel<%d, false, %s, false>" % (d, "true" if info["split"] else "false")
+    if stage == "decode":
+        kv = wl.seq_lens + (1 if s.decode_steps else 0)  # the first of the fused decode steps
+        info = tide.tide_plan_info_get(tide.TIDE_OP_DECODE, kv, None, dims)
+        return "decode_split_kernel<%d, false, %s, %d>%s" % (
+            d, "true" if s.decode_steps else "false", info["waves_per_group"],
+            " (merge in kernel)" if info["merge_in_kernel"] else " + decode_merge_kernel")
+    return "decode_split_kernel<%d, true, false, 4|8 by item count> + decode_merge_kernel" % d
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -730,9 +750,7 @@ def main():
     primary = ("extend" if "extend" in rooflines else
                "shared_decode" if "shared_decode" in rooflines else "decode")
     roofline = dict(rooflines[primary])
-    roofline["kernel"] = {"extend": "extend_attn_kernel<128, false, false>",
-                          "decode": "decode_split_kernel<128, false, false, 8>",
-                          "shared_decode": "decode_split_kernel<128, true, false, 8>"}[primary]
+    roofline["kernel"] = kernel_label(wl, primary)
     roofline["traffic"] = counter_traffic(s.key, primary)
 
     cpu = None

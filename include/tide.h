@@ -129,6 +129,21 @@ typedef struct tide_dims {
 TIDE_API int tide_workspace_size(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* lens_b,
                         const tide_dims* dims, int32_t num_splits, size_t* bytes_out);
 
+/* The launch a call with these arguments makes (diagnostics: which kernel variant runs,
+ * and how the work is cut).  Same arguments as tide_workspace_size; fills *out. */
+typedef struct tide_plan_info {
+  int32_t num_items;        /* work items (workgroups for extend/prefill, waves for decode) */
+  int32_t waves_per_group;  /* waves per workgroup of the main kernel */
+  int32_t split;            /* extend/prefill: 1 when split-KV chunks and a merge run */
+  int32_t max_splits;       /* decode: the most splits of any task */
+  int32_t merge_in_kernel;  /* decode: 1 when the split kernel merges (no merge kernel) */
+  int32_t reserved;
+  size_t workspace_bytes;
+} tide_plan_info;
+TIDE_API int tide_plan_info_get(int op, int32_t num_tasks, const int32_t* lens_a,
+                        const int32_t* lens_b, const tide_dims* dims, int32_t num_splits,
+                        tide_plan_info* out);
+
 /*
  * KV-append: store the K/V of each task's new tokens into its pages (the retained
  * state that Continuous Task Batching keeps resident, Section 4).

@@ -14,7 +14,7 @@ from ._lib import (TIDE_ERR_CAPACITY, TIDE_ERR_HIP, TIDE_ERR_INVALID_ARG, TIDE_E
                    tide_decode_attn_noalloc, NOALLOC_SCRATCH_BYTES, tide_extend_append_attn,
                    tide_decode_attn_shared, tide_dims,
                    tide_extend_attn, tide_full_prefill_attn, tide_kv_append, tide_shutdown,
-                   tide_workspace_size, tide_workspace_size_shared)
+                   tide_plan_info_get, tide_workspace_size, tide_workspace_size_shared)
 from .kvcache import PagedKV
 
 __all__ = ["TIDE_ERR_CAPACITY", "TIDE_ERR_HIP", "TIDE_ERR_INVALID_ARG", "TIDE_ERR_PAGE_RANGE",
@@ -24,4 +24,4 @@ __all__ = ["TIDE_ERR_CAPACITY", "TIDE_ERR_HIP", "TIDE_ERR_INVALID_ARG", "TIDE_ER
            "tide_full_prefill_attn", "tide_kv_append", "tide_shutdown", "tide_workspace_size",
            "tide_decode_attn_shared", "tide_workspace_size_shared", "tide_decode_append_attn",
            "tide_decode_attn_noalloc", "NOALLOC_SCRATCH_BYTES", "tide_extend_append_attn",
-           "PagedKV"]
+           "tide_plan_info_get", "PagedKV"]

@@ -33,7 +33,7 @@ NOALLOC_SCRATCH_BYTES = 64 << 20
 EXPORTED = ("tide_workspace_size", "tide_kv_append", "tide_extend_attn", "tide_decode_attn",
             "tide_full_prefill_attn", "tide_decode_attn_shared", "tide_workspace_size_shared",
             "tide_decode_append_attn", "tide_decode_attn_noalloc", "tide_extend_append_attn",
-            "tide_ctb_create", "tide_ctb_step", "tide_ctb_get_stats", "tide_ctb_destroy",
+            "tide_plan_info_get", "tide_ctb_create", "tide_ctb_step", "tide_ctb_get_stats", "tide_ctb_destroy",
             "tide_status_string", "tide_shutdown")
 
 
@@ -47,6 +47,13 @@ class tide_dims(ctypes.Structure):
     _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32),
                 ("sm_scale", ctypes.c_float)]
+
+
+class tide_plan_info(ctypes.Structure):
+    _fields_ = [("num_items", ctypes.c_int32), ("waves_per_group", ctypes.c_int32),
+                ("split", ctypes.c_int32), ("max_splits", ctypes.c_int32),
+                ("merge_in_kernel", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("workspace_bytes", ctypes.c_size_t)]
 
 
 def make_dims(num_q_heads: int, num_kv_heads: int, head_dim: int, sm_scale: float,
@@ -87,6 +94,8 @@ def load(path: str = LIB_PATH):
                                             i32, vp, vp, vp, sz, vp]
     lib.tide_workspace_size_shared.argtypes = [i32, vp, i32, vp, vp, dims_p, i32,
                                                ctypes.POINTER(sz)]
+    lib.tide_plan_info_get.argtypes = [ctypes.c_int, i32, vp, vp, dims_p, i32,
+                                       ctypes.POINTER(tide_plan_info)]
     lib.tide_ctb_create.argtypes = [vp, i32, vp, vp, i32, vp, vp, vp, vp, vp,
                                     ctypes.POINTER(vp)]
     lib.tide_ctb_step.argtypes = [vp, vp]
@@ -213,6 +222,17 @@ def tide_workspace_size(op: int, lens_a, lens_b, dims: tide_dims, num_splits: in
     _check(load().tide_workspace_size(op, n, a_p, b_p, ctypes.byref(dims), int(num_splits),
                                       ctypes.byref(out)), "tide_workspace_size")
     return int(out.value)
+
+
+def tide_plan_info_get(op: int, lens_a, lens_b, dims: tide_dims, num_splits: int = 0) -> dict:
+    """The launch a call with these lengths makes (items, waves per workgroup, ...)."""
+    a, a_p = _host(lens_a, "lens_a")
+    b, b_p = _host(lens_b, "lens_b")
+    n = 0 if a is None else int(a.size)
+    info = tide_plan_info()
+    _check(load().tide_plan_info_get(op, n, a_p, b_p, ctypes.byref(dims), int(num_splits),
+                                     ctypes.byref(info)), "tide_plan_info_get")
+    return {name: getattr(info, name) for name, _ in tide_plan_info._fields_ if name != "reserved"}
 
 
 def alloc_workspace(nbytes: int, device="cuda") -> torch.Tensor:

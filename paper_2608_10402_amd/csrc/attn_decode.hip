@@ -584,7 +584,7 @@ __global__ __launch_bounds__(kMergeWaves * 64) void decode_merge_kernel(DecodeAr
 template <int D, bool kShared, bool kAppend>
 hipError_t launch(const DecodeArgs& a, hipStream_t stream) {
   if (a.num_items > 0) {
-    if (a.num_items >= kBigLaunchItems) {
+    if (decode_waves(a.num_items) == kBigWaves) {
       const int blocks = (a.num_items + kBigWaves - 1) / kBigWaves;
       hipLaunchKernelGGL((decode_split_kernel<D, kShared, kAppend, kBigWaves>), dim3(blocks),
                          dim3(kBigWaves * 64), 0, stream, a);
@@ -623,6 +623,10 @@ template __global__ void decode_split_kernel<64, false, true, kBigWaves>(DecodeA
 template __global__ void decode_split_kernel<64, false, true, kSmallWaves>(DecodeArgs);
 
 }  // namespace kern
+
+int decode_waves(int32_t num_items) {
+  return num_items >= kern::kBigLaunchItems ? kern::kBigWaves : kern::kSmallWaves;
+}
 
 hipError_t launch_decode(const DecodeArgs& a, int head_dim, bool shared, hipStream_t stream) {
   const bool append = a.k_new != nullptr;

@@ -16,5 +16,8 @@ namespace kern {
 hipError_t launch_extend_append_attn(const ExtendArgs& a, int head_dim, hipStream_t stream);
 }  // namespace kern
 hipError_t launch_decode(const DecodeArgs& a, int head_dim, bool shared, hipStream_t stream);
+// Waves per workgroup the decode split kernel and the append kernel launch with.
+int decode_waves(int32_t num_items);
+int append_waves();
 
 }  // namespace tide

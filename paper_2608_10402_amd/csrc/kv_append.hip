@@ -70,6 +70,8 @@ hipError_t launch(const AppendArgs& a, hipStream_t stream) {
 
 }  // namespace kern
 
+int append_waves() { return kern::kWaves; }
+
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream) {
   if (a.num_items == 0) return hipSuccess;
   if (a.head_dim == 128) return kern::launch<128>(a, stream);

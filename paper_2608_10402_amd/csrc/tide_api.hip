@@ -281,6 +281,35 @@ TIDE_API int tide_workspace_size(int op, int32_t num_tasks, const int32_t* lens_
   }
 }
 
+TIDE_API int tide_plan_info_get(int op, int32_t num_tasks, const int32_t* lens_a,
+                               const int32_t* lens_b, const tide_dims* dims, int32_t num_splits,
+                               tide_plan_info* out) {
+  try {
+    if (!out) return TIDE_ERR_INVALID_ARG;
+    int rc = check_dims(dims);
+    if (rc != TIDE_OK) return rc;
+    Plan plan;
+    rc = make_plan(op, num_tasks, lens_a, lens_b, *dims, num_splits, -1, false, &plan);
+    if (rc != TIDE_OK) return rc;
+    *out = tide_plan_info{};
+    out->num_items = plan.num_items;
+    out->workspace_bytes = plan.total_bytes;
+    if (op == TIDE_OP_DECODE) {
+      out->waves_per_group = decode_waves(plan.num_items);
+      out->max_splits = plan.max_splits;
+      out->merge_in_kernel = plan.fold_merge ? 1 : 0;
+    } else if (op == TIDE_OP_KV_APPEND) {
+      out->waves_per_group = append_waves();
+    } else {
+      out->waves_per_group = plan.waves;
+      out->split = plan.split ? 1 : 0;
+    }
+    return TIDE_OK;
+  } catch (...) {
+    return TIDE_ERR_HIP;
+  }
+}
+
 TIDE_API int tide_kv_append(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
                             int64_t num_pages, const int32_t* block_table, int32_t bt_stride,
                             int32_t num_tasks, const int32_t* prefix_lens,

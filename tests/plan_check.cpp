@@ -1,10 +1,14 @@
-// Host-side checker of the extend / prefill work lists built by the planner (plan.cpp),
-// compiled with g++ by test_plan.py; no GPU involved.
+// Host-side checker of the work lists built by the planner (plan.cpp), compiled with g++
+// by test_plan.py; no GPU involved.
 //
 // Each stdin line is one call: "op hq hkv d ntasks p_0 e_0 p_1 e_1 ..." (op 2 = extend,
-// 4 = full prefill, which reads e_i as the sequence length and ignores p_i).  For every
-// call the checker builds the plan, reads the uploaded blob back and verifies what the
-// kernels assume:
+// 4 = full prefill, which reads e_i as the sequence length and ignores p_i), or
+// "3 hq hkv d ntasks num_splits kv_0 .. kv_{n-1}" (decode), or
+// "100 hq hkv d ntasks num_splits ngroups gs_0 .. gs_ngroups sh_0 .. kv_0 .." (decode with
+// shared group prefixes; gs = group starts, sh = shared prefix lengths).  Decode calls are
+// checked by check_decode / check_shared below.  For every extend / prefill call the
+// checker builds the plan, reads the uploaded blob back and verifies what the kernels
+// assume:
 //   * every (task, kv head, token) row block is covered by exactly one item, and every
 //     item's tokens lie inside its task;
 //   * split plan: the chunks of each (block, kv head) partition the key tiles the block
@@ -150,6 +154,148 @@ static int check(int op, const tide_dims& dims, const std::vector<int32_t>& pa,
   return 0;
 }
 
+// Regions of a decode workspace: tasks, items, then (plain decode) the arrival counters,
+// all inside the upload; the partial buffers after it, large enough for every
+// (task, query head, split) slot.
+static int check_decode_layout(const Plan& plan, const tide_dims& dims, int32_t n,
+                               size_t item_size, bool counters) {
+  if (plan.blob.size() != plan.upload_bytes) return fail("blob size");
+  if (plan.items_off < plan.tasks_off + (size_t)n * sizeof(TaskDesc)) return fail("items overlap tasks");
+  const size_t items_end = plan.items_off + (size_t)plan.num_items * item_size;
+  if (items_end > plan.upload_bytes) return fail("items beyond upload");
+  if (counters) {
+    if (plan.tickets_off < items_end) return fail("counters overlap items");
+    const size_t end = plan.tickets_off + (size_t)n * dims.num_kv_heads * sizeof(int32_t);
+    if (end > plan.upload_bytes) return fail("counters beyond upload");
+    for (size_t i = plan.tickets_off; i < end; ++i)
+      if (plan.blob[i] != 0) return fail("counter not zero", (long)i);
+  }
+  const size_t slots = (size_t)n * dims.num_q_heads * (size_t)plan.max_splits;
+  if (plan.part_o_off < plan.upload_bytes) return fail("partials overlap upload");
+  if (plan.part_ml_off < plan.part_o_off + slots * dims.head_dim * 4) return fail("part_o size");
+  if (plan.total_bytes < plan.part_ml_off + slots * 16) return fail("part_ml size");
+  if (plan.part_o_off % 16 || plan.part_ml_off % 16) return fail("partial alignment");
+  return 0;
+}
+
+// Plain decode: every (task, kv head) is cut into chunks of plan.chunk keys, split s
+// covering keys [s * chunk, min(kv, (s + 1) * chunk)); each (task, kv head, split) is one
+// item; the task table holds kv - 1 + 1 and the split count; full chunks come first, then
+// the shorter last chunks, longest first; the in-kernel merge is chosen at <= 4 splits
+// per task on average.
+static int check_decode(const tide_dims& dims, int32_t num_splits, const std::vector<int32_t>& kv) {
+  const int32_t n = (int32_t)kv.size();
+  Plan plan, sized;
+  int rc = make_plan(TIDE_OP_DECODE, n, kv.data(), nullptr, dims, num_splits, -1, true, &plan);
+  if (rc != TIDE_OK) return fail("make_plan", rc);
+  rc = make_plan(TIDE_OP_DECODE, n, kv.data(), nullptr, dims, num_splits, -1, false, &sized);
+  if (rc != TIDE_OK || sized.total_bytes != plan.total_bytes || sized.fold_merge != plan.fold_merge)
+    return fail("size-only plan differs");
+  if (check_decode_layout(plan, dims, n, sizeof(DecodeItem), true)) return 1;
+  const int64_t chunk = plan.chunk;
+  if (chunk < kDecodeStep || chunk % kDecodeStep) return fail("chunk", (long)chunk);
+  const int32_t Hkv = dims.num_kv_heads;
+  const TaskDesc* tasks = reinterpret_cast<const TaskDesc*>(plan.blob.data() + plan.tasks_off);
+  int32_t max_splits = 0;
+  for (int32_t b = 0; b < n; ++b) {
+    const int32_t want = (int32_t)((kv[b] + chunk - 1) / chunk);
+    if (tasks[b].row_start != b || tasks[b].prefix + tasks[b].extend != kv[b] ||
+        tasks[b].extend != 1 || tasks[b].aux != want)
+      return fail("task row", b, tasks[b].aux);
+    max_splits = std::max(max_splits, want);
+  }
+  if (plan.max_splits != max_splits) return fail("max splits", plan.max_splits, max_splits);
+  std::set<std::tuple<int, int, int>> seen;
+  const DecodeItem* items = reinterpret_cast<const DecodeItem*>(plan.blob.data() + plan.items_off);
+  int64_t prev_len = chunk;
+  bool in_tail = false;
+  for (int32_t i = 0; i < plan.num_items; ++i) {
+    const DecodeItem it = items[i];
+    if (it.task < 0 || it.task >= n || it.kv_head < 0 || it.kv_head >= Hkv) return fail("item ids", i);
+    if (it.split < 0 || it.split >= tasks[it.task].aux) return fail("split id", i, it.split);
+    if ((int64_t)it.k_begin != it.split * chunk) return fail("k_begin", i, it.k_begin);
+    if (!seen.insert({it.task, it.kv_head, it.split}).second) return fail("item twice", i);
+    const int64_t len = std::min<int64_t>(chunk, kv[it.task] - it.k_begin);
+    if (len <= 0) return fail("empty item", i);
+    if (len < chunk) in_tail = true;
+    else if (in_tail) return fail("full chunk after a tail chunk", i);
+    if (in_tail && len > prev_len) return fail("tail not longest first", i);
+    prev_len = len;
+  }
+  int64_t want_items = 0;
+  for (int32_t b = 0; b < n; ++b) want_items += (int64_t)tasks[b].aux * Hkv;
+  if ((int64_t)plan.num_items != want_items || (int64_t)seen.size() != want_items)
+    return fail("item count", plan.num_items, (long)want_items);
+  if (plan.fold_merge != (plan.num_items <= 4 * (int64_t)n * Hkv)) return fail("fold choice");
+  printf("ok %d %lld %d %d %zu\n", plan.num_items, (long long)chunk, plan.max_splits,
+         plan.fold_merge ? 1 : 0, plan.total_bytes);
+  return 0;
+}
+
+// Shared-prefix decode: for every task and kv head, the items that cover it (prompt
+// chunks of its group, read once for up to 16 / G trajectories, then its own chunks)
+// give split ids 0 .. aux-1 exactly once and key ranges that tile [0, kv) in split
+// order; a prompt item stays inside the prompt and its group, an own item after the
+// prompt; every item fits the 16 MFMA columns; items are ordered longest first.
+static int check_shared(const tide_dims& dims, int32_t num_splits, const std::vector<int32_t>& kv,
+                        const std::vector<int32_t>& gs, const std::vector<int32_t>& sh) {
+  const int32_t n = (int32_t)kv.size(), ng = (int32_t)sh.size();
+  Plan plan, sized;
+  int rc = make_plan_shared(n, kv.data(), ng, gs.data(), sh.data(), dims, num_splits, -1, true, &plan);
+  if (rc != TIDE_OK) return fail("make_plan_shared", rc);
+  rc = make_plan_shared(n, kv.data(), ng, gs.data(), sh.data(), dims, num_splits, -1, false, &sized);
+  if (rc != TIDE_OK || sized.total_bytes != plan.total_bytes) return fail("size-only plan differs");
+  if (check_decode_layout(plan, dims, n, sizeof(SharedDecodeItem), false)) return 1;
+  const int32_t Hkv = dims.num_kv_heads, G = dims.num_q_heads / dims.num_kv_heads;
+  const TaskDesc* tasks = reinterpret_cast<const TaskDesc*>(plan.blob.data() + plan.tasks_off);
+  std::vector<int32_t> group_of(n), shared_of(n);
+  for (int32_t g = 0; g < ng; ++g)
+    for (int32_t b = gs[g]; b < gs[g + 1]; ++b) group_of[b] = g, shared_of[b] = sh[g];
+  // (task, kv head) -> split -> key range
+  std::map<std::pair<int, int>, std::map<int, std::pair<int, int>>> cover;
+  const SharedDecodeItem* items =
+      reinterpret_cast<const SharedDecodeItem*>(plan.blob.data() + plan.items_off);
+  int prev_len = INT32_MAX;
+  for (int32_t i = 0; i < plan.num_items; ++i) {
+    const SharedDecodeItem it = items[i];
+    if (it.first_task < 0 || it.ntasks < 1 || it.first_task + it.ntasks > n) return fail("item tasks", i);
+    if (it.ntasks * G > 16) return fail("item columns", i, it.ntasks);
+    if (it.kv_head < 0 || it.kv_head >= Hkv) return fail("item head", i);
+    if (it.k_begin < 0 || it.k_end <= it.k_begin) return fail("item keys", i);
+    const int g = group_of[it.first_task];
+    if (group_of[it.first_task + it.ntasks - 1] != g) return fail("item spans groups", i);
+    const bool prompt = it.k_end <= sh[g] && it.split < (sh[g] + plan.chunk - 1) / plan.chunk;
+    if (!prompt && (it.ntasks != 1 || it.k_begin < sh[g])) return fail("own item", i);
+    const int len = it.k_end - it.k_begin;
+    if (len > prev_len) return fail("not longest first", i);
+    prev_len = len;
+    for (int t = it.first_task; t < it.first_task + it.ntasks; ++t) {
+      if (it.k_end > kv[t]) return fail("item past context", i, t);
+      auto& m = cover[{t, it.kv_head}];
+      if (!m.insert({it.split, {it.k_begin, it.k_end}}).second) return fail("split twice", t, it.split);
+    }
+  }
+  int32_t max_splits = 0;
+  for (int32_t b = 0; b < n; ++b) {
+    if (tasks[b].row_start != b) return fail("row_start", b);
+    max_splits = std::max(max_splits, tasks[b].aux);
+    for (int32_t h = 0; h < Hkv; ++h) {
+      const auto& m = cover[{b, h}];
+      if ((int)m.size() != tasks[b].aux) return fail("split count", b, (long)m.size());
+      int at = 0, s = 0;
+      for (const auto& kvp : m) {
+        if (kvp.first != s++) return fail("split ids", b, kvp.first);
+        if (kvp.second.first != at) return fail("key gap", b, at);
+        at = kvp.second.second;
+      }
+      if (at != kv[b]) return fail("keys end", b, at);
+    }
+  }
+  if (plan.max_splits < max_splits) return fail("max splits", plan.max_splits, max_splits);
+  printf("ok %d %d %d %zu\n", plan.num_items, plan.chunk, plan.max_splits, plan.total_bytes);
+  return 0;
+}
+
 int main() {
   std::string line;
   int bad = 0;
@@ -157,16 +303,32 @@ int main() {
     std::istringstream in(line);
     int op, hq, hkv, d, n;
     if (!(in >> op >> hq >> hkv >> d >> n)) continue;
-    std::vector<int32_t> pa(n), pb(n);
-    for (int i = 0; i < n; ++i) in >> pa[i] >> pb[i];
     tide_dims dims = {};
     dims.num_q_heads = hq;
     dims.num_kv_heads = hkv;
     dims.head_dim = d;
     dims.page_size = 16;
     dims.sm_scale = 0.088f;
-    if (op == TIDE_OP_FULL_PREFILL) pa = pb;
-    bad |= check(op, dims, pa, pb);
+    if (op == TIDE_OP_DECODE || op == kOpDecodeShared) {
+      int splits = 0, ng = 0;
+      in >> splits;
+      std::vector<int32_t> gs, sh;
+      if (op == kOpDecodeShared) {
+        in >> ng;
+        gs.resize(ng + 1);
+        sh.resize(ng);
+        for (auto& x : gs) in >> x;
+        for (auto& x : sh) in >> x;
+      }
+      std::vector<int32_t> kv(n);
+      for (auto& x : kv) in >> x;
+      bad |= op == TIDE_OP_DECODE ? check_decode(dims, splits, kv) : check_shared(dims, splits, kv, gs, sh);
+    } else {
+      std::vector<int32_t> pa(n), pb(n);
+      for (int i = 0; i < n; ++i) in >> pa[i] >> pb[i];
+      if (op == TIDE_OP_FULL_PREFILL) pa = pb;
+      bad |= check(op, dims, pa, pb);
+    }
     fflush(stdout);
   }
   return bad;

@@ -320,3 +320,30 @@ def test_binding_checks_row_counts_before_the_call():
         tide.tide_decode_attn_shared(torch.zeros(3, 8, 64, dtype=torch.bfloat16), kp, vp, bt,
                                      [6, 10, 7], [0, 3], [0], dims,
                                      torch.zeros(3, 8, 64, dtype=torch.bfloat16))
+
+
+def test_plan_info_matches_workspace_size_and_launch_rules():
+    """tide_plan_info_get reports the same workspace as tide_workspace_size, 8-wave decode
+    workgroups from 2,048 items on (4 below), and the in-kernel merge at <= 4 splits per
+    task on average (no GPU needed: planning is host code)."""
+    import paper_2608_10402_amd as tide
+    dims = tide.make_dims(32, 8, 128, 0.088)
+    for kv, waves in (([100] * 8, 4), ([5000] * 256, 8)):
+        kv = np.asarray(kv, np.int32)
+        info = tide.tide_plan_info_get(tide.TIDE_OP_DECODE, kv, None, dims)
+        assert info["workspace_bytes"] == tide.tide_workspace_size(tide.TIDE_OP_DECODE, kv, None, dims)
+        assert info["waves_per_group"] == waves
+        assert info["merge_in_kernel"] == int(info["num_items"] <= 4 * kv.size * 8)
+    one = tide.tide_plan_info_get(tide.TIDE_OP_DECODE, np.asarray([64] * 4, np.int32), None, dims,
+                                  num_splits=1)
+    many = tide.tide_plan_info_get(tide.TIDE_OP_DECODE, np.asarray([9000] * 4, np.int32), None,
+                                   dims, num_splits=40)
+    assert one["max_splits"] == 1 and one["merge_in_kernel"] == 1
+    # 40 splits asked: chunks of ceil(9000 / 40) keys rounded up to 32 -> 256 -> 36 splits
+    assert many["max_splits"] == 36 and many["merge_in_kernel"] == 0
+    p, e = np.asarray([1000, 20], np.int32), np.asarray([300, 5], np.int32)
+    info = tide.tide_plan_info_get(tide.TIDE_OP_EXTEND, p, e, dims)
+    assert info["workspace_bytes"] == tide.tide_workspace_size(tide.TIDE_OP_EXTEND, p, e, dims)
+    assert info["waves_per_group"] == 8 and info["num_items"] > 0
+    with pytest.raises(tide.TideError):
+        tide.tide_plan_info_get(tide.TIDE_OP_DECODE, np.asarray([0], np.int32), None, dims)

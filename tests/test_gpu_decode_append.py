@@ -41,6 +41,9 @@ CASES = {
                                                [1] * 7, seed=21),
     "edges_g16_d64": lambda: W.custom_workload(16, 1, 64, [0, 15, 16, 500], [1] * 4, seed=22),
     "g1_d128": lambda: W.custom_workload(4, 4, 128, [47, 3, 300], [1] * 3, seed=23),
+    # d = 64 with 2,048+ work items, so the 8-wave workgroups of large launches run
+    "d64_2k_items": lambda: W.custom_workload(16, 2, 64, [2000 + 7 * (i % 40) for i in range(256)],
+                                              [1] * 256, seed=25),
 }
 
 

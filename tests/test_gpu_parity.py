@@ -128,6 +128,10 @@ DECODE_WORKLOADS = {
                                                  [1] * 8, seed=5),
     "decode_g16_d64": lambda: W.custom_workload(16, 1, 64, [0, 100, 999], [1, 1, 1], seed=6),
     "decode_g1": lambda: W.custom_workload(4, 4, 128, [3000, 1], [1, 1], seed=7),
+    # d = 64 with 2,048+ work items, so the 8-wave workgroups of large launches run
+    "decode_d64_2k_items": lambda: W.custom_workload(16, 2, 64,
+                                                     [2000 + 7 * (i % 40) for i in range(256)],
+                                                     [1] * 256, seed=8),
 }
 
 

@@ -29,6 +29,9 @@ WORKLOADS = {
                                                       [1, 20, 300, 1, 5], seed=4),
     "groups_g1_16wide": lambda: W.custom_group_workload(4, 4, 128, [16, 5], [2048, 0],
                                                         [1] * 8 + [3] * 8 + [100] * 5, seed=5),
+    # d = 64 with 2,048+ work items, so the 8-wave workgroups of large launches run
+    "groups_d64_2k_items": lambda: W.custom_group_workload(
+        16, 2, 64, [8] * 64, [1024] * 64, [1 + (37 * i) % 1500 for i in range(512)], seed=6),
 }
 
 

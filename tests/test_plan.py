@@ -99,3 +99,71 @@ def test_split_choice(checker):
     # the split plan's workspace adds the fp32 partials
     assert int(auto[0][4]) > int(plain[0][4])
     assert auto[2][2:5] == plain[2][2:5]
+
+
+OP_DECODE, OP_SHARED = 3, 100
+
+
+def _decode_line(hq, hkv, d, kv, splits=0):
+    return "%d %d %d %d %d %d %s" % (OP_DECODE, hq, hkv, d, len(kv), splits,
+                                     " ".join(str(int(x)) for x in kv))
+
+
+def _shared_line(hq, hkv, d, kv, group_start, shared, splits=0):
+    return "%d %d %d %d %d %d %d %s %s %s" % (
+        OP_SHARED, hq, hkv, d, len(kv), splits, len(shared),
+        " ".join(str(int(x)) for x in group_start), " ".join(str(int(x)) for x in shared),
+        " ".join(str(int(x)) for x in kv))
+
+
+def test_decode_plans_are_valid(checker):
+    """Plain decode work lists: every (task, kv head) chunked exactly once in split order,
+    full chunks before the shorter last ones (longest first), the merge mode as the rule
+    says, counters zeroed in the upload, partial buffers sized for every slot."""
+    rng = np.random.default_rng(5)
+    heads = [(28, 4), (32, 8), (8, 8), (16, 1), (64, 8), (12, 4)]
+    lines = []
+    for i in range(120):
+        hq, hkv = heads[rng.integers(len(heads))]
+        d = int(rng.choice([64, 128]))
+        n = int(rng.choice([1, 2, 7, 64, 256, 600]))
+        scale = int(rng.choice([40, 1000, 8000, 60000]))
+        kv = rng.integers(1, scale, size=n)
+        splits = int(rng.choice([0, 0, 1, 2, 3, 7, 64]))
+        lines.append(_decode_line(hq, hkv, d, kv, splits))
+    lines += [
+        _decode_line(28, 4, 128, [1]),                    # a lone first token
+        _decode_line(32, 8, 128, [32, 33, 64, 4064, 4065]),
+        _decode_line(16, 1, 64, [2_000_000]),             # chunk at its cap
+        _decode_line(32, 8, 128, [16384] * 256),          # every chunk full
+        _decode_line(32, 8, 128, [5] * 2048),             # one split each: direct writes
+        _decode_line(8, 8, 64, [100, 3000], splits=100),  # more splits asked than keys
+    ]
+    out = _run(checker, lines)
+    folds = [int(o[4]) for o in out]
+    assert 0 in folds and 1 in folds  # both merge modes are exercised
+
+
+def test_shared_decode_plans_are_valid(checker):
+    """Shared-prefix decode work lists: per task and kv head the prompt chunks of its
+    group and its own chunks give each split id once and tile [0, kv) in order; prompt
+    items stay inside one group and 16 MFMA columns."""
+    rng = np.random.default_rng(6)
+    lines = []
+    for i in range(80):
+        hq, hkv = [(32, 8), (28, 4), (16, 1), (64, 8), (8, 8)][rng.integers(5)]
+        d = int(rng.choice([64, 128]))
+        ng = int(rng.choice([1, 2, 5, 16]))
+        sizes = rng.integers(1, 9, size=ng)
+        gs = np.concatenate([[0], np.cumsum(sizes)])
+        shared = 16 * rng.integers(0, int(rng.choice([2, 60, 500])), size=ng)
+        kv = np.concatenate([s + rng.integers(1, int(rng.choice([2, 300, 5000])), size=k)
+                             for s, k in zip(shared, sizes)])
+        splits = int(rng.choice([0, 0, 1, 4, 32]))
+        lines.append(_shared_line(hq, hkv, d, kv, gs, shared, splits))
+    lines += [
+        _shared_line(32, 8, 128, [17, 17], [0, 2], [16]),          # one key past the prompt
+        _shared_line(16, 1, 128, [1, 1, 1], [0, 3], [0]),          # no prompt at all
+        _shared_line(8, 8, 64, [100001] * 4, [0, 4], [100000 // 16 * 16]),
+    ]
+    _run(checker, lines)
