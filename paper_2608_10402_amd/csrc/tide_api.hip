@@ -89,7 +89,7 @@ int upload(const Plan& plan, void* workspace, hipStream_t stream) {
   DeviceStaging& ds = *g_staging[dev];
   StagingSlot& s = ds.slots[ds.next];
   ds.next = (ds.next + 1) % kStagingSlots;
-  if (!s.done && hipEventCreateWithFlags(&s.done, hipEventDisableTiming) != hipSuccess)
+  if (!s.done && hipEventCreateWithFlags(&s.done, hipEventDisableTiming | hipEventDisableSystemFence) != hipSuccess)
     return TIDE_ERR_HIP;
   if (s.pending) {
     if (hipEventSynchronize(s.done) != hipSuccess) return TIDE_ERR_HIP;
