@@ -280,6 +280,25 @@ void extend_attn_kernel(ExtendArgs a) {
       dma16_lane(src, buf + lds_row0 + i * 1024);
     }
   };
+  // A tile whose keys all lie at or past P (and below seq_len, or zero-filled past it) is
+  // streamed from the caller's new rows with the same buffer loads as a pool page: the
+  // buffer starts at the tile's first key's row of this kv head, rows are
+  // num_kv_heads * D * 2 bytes apart, and lane offsets are constants like the page path's.
+  const int64_t new_stride = (int64_t)a.num_kv_heads * S::kRowBytes;  // bytes per token row
+  auto one_new = [&](int t, const uint16_t* rows, bool is_v, uint8_t* buf) {
+    const int t0 = (tbase + t) * 64;             // first key of the tile, >= P
+    const int n = min(seq_len - t0, 64);         // its rows among the new rows (>= 1)
+    const uint8_t* base =
+        reinterpret_cast<const uint8_t*>(rows + (new_row0 + (int64_t)(t0 - P) * a.num_kv_heads) * D);
+    const int bytes = (int)((n - 1) * new_stride) + S::kRowBytes;  // rows past n read as 0
+#pragma unroll
+    for (int i = 0; i < S::kDma; ++i) {
+      const int r = 8 * wave + i * S::kRowsPerDma + lane / S::kNG;  // tile row
+      const int p = lane % S::kNG;
+      const int g = is_v ? (p ^ (vseg<D>(r) << 2)) : kswz<D>(r, p);  // logical granule
+      dma16(base, bytes, (uint32_t)(r * (int)new_stride + g * 16), buf + lds_row0 + i * 1024);
+    }
+  };
   // The V tile's loads go first: a wait can then cover a group's V tile without its K tile.
   // tk / tv: the local tiles loaded (only used by the fused path).  With fuse_tag false the
   // caller guarantees that both tiles lie below the prefix, and no fused code is emitted.
@@ -297,15 +316,20 @@ void extend_attn_kernel(ExtendArgs a) {
 #pragma unroll
       for (int i = 0; i < S::kDma; ++i) dma16(pool + blk, bytes, src[i], buf + lds_row0 + i * 1024);
     };
-    // a tile past the item keeps the zero-length path (its keys are never used)
-    if (kFuse && tv < ntiles && (tbase + tv + 1) * 64 > P)
-      one_fused(tv, vword, vpool, a.v_new, true, vbuf);
-    else
+    // a tile past the item keeps the zero-length path (its keys are never used); a tile
+    // wholly at or past P reads the new rows, the one holding key P mixes both sources
+    if (kFuse && tv < ntiles && (tbase + tv + 1) * 64 > P) {
+      if ((tbase + tv) * 64 >= P) one_new(tv, a.v_new, true, vbuf);
+      else one_fused(tv, vword, vpool, a.v_new, true, vbuf);
+    } else {
       one(vword, vpool, v_src, vbuf);
-    if (kFuse && tk < ntiles && (tbase + tk + 1) * 64 > P)
-      one_fused(tk, kword, kpool, a.k_new, false, kbuf);
-    else
+    }
+    if (kFuse && tk < ntiles && (tbase + tk + 1) * 64 > P) {
+      if ((tbase + tk) * 64 >= P) one_new(tk, a.k_new, false, kbuf);
+      else one_fused(tk, kword, kpool, a.k_new, false, kbuf);
+    } else {
       one(kword, kpool, k_src, kbuf);
+    }
   };
   const std::true_type fuse;  // streams that may cross the prefix (fused variant only)
 
