@@ -74,6 +74,9 @@ PROFILE_SUMMARIES = {
     ("multimodal_resume", "extend"): "attn_extend_multimodal_resume_counters.txt",
     ("long_horizon", "extend"): "attn_extend_long_horizon_counters.txt",
     ("long_horizon", "decode"): "decode_split_long_horizon_counters.txt",
+    ("agent_resume_7b", "decode"): "decode_split_agent_resume_7b_counters.txt",
+    ("multimodal_resume", "decode"): "decode_split_multimodal_resume_counters.txt",
+    ("multimodal_prune_resume", "decode"): "decode_split_multimodal_prune_resume_counters.txt",
 }
 
 
@@ -757,6 +760,8 @@ def main():
     roofline = dict(rooflines[primary])
     roofline["kernel"] = kernel_label(wl, primary)
     roofline["traffic"] = counter_traffic(s.key, primary)
+    for name, r in rooflines.items():  # HBM bytes per launch of each stage's kernel, where a summary exists
+        r["traffic"] = counter_traffic(s.key, name)
 
     cpu = None
     if args.cpu_seconds > 0 and "extend" in ms:
