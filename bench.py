@@ -83,7 +83,7 @@ PROFILE_SUMMARIES = {
 def parse_args():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="agent_resume_7b")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -655,7 +655,9 @@ def main():
     # kernel boundary imprecisely, so they are not used for the per-stage figures.
     # A stage that moves less than 1 GB could be served from the 256 MB MALL and the L2s
     # when repeated back to back, so it is timed call by call, with 512 MB of scratch
-    # overwritten between calls (outside the events).
+    # overwritten between calls (outside the events).  The other stages are also timed
+    # call by call after their back-to-back run; the median and minimum of the per-call
+    # times are reported beside the back-to-back mean, which the rates use.
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     for st in stages:
         if st.flops == 0 and st.bytes < 1e9:
@@ -668,7 +670,8 @@ def main():
                 eb.record(stream)
                 evs.append((ea, eb))
             torch.cuda.synchronize()
-            st.times.append(sum(a_.elapsed_time(b_) for a_, b_ in evs) / args.steps)
+            st.per_call = [a_.elapsed_time(b_) for a_, b_ in evs]
+            st.times.append(sum(st.per_call) / args.steps)
             st.flushed = True
             continue
         ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -678,6 +681,16 @@ def main():
         eb.record(stream)
         torch.cuda.synchronize()
         st.times.append(ea.elapsed_time(eb) / args.steps)
+        # the same calls one by one under their own events, for the median and the minimum
+        evs = []
+        for _ in range(args.steps):
+            ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            ea.record(stream)
+            st.fn()
+            eb.record(stream)
+            evs.append((ea, eb))
+        torch.cuda.synchronize()
+        st.per_call = [a_.elapsed_time(b_) for a_, b_ in evs]
     del flush
     ms = {st.name: float(np.mean(st.times)) for st in stages}
 
@@ -686,7 +699,11 @@ def main():
         return (sum(np.mean(st.times) for st in sel), sum(st.flops for st in sel),
                 sum(st.bytes for st in sel))
 
-    extra = {"stage_ms": {k: round(v, 4) for k, v in ms.items()}, "setup_s": round(setup_s, 1),
+    extra = {"stage_ms": {k: round(v, 4) for k, v in ms.items()},
+             "stage_ms_median_min": {st.name: [round(float(np.median(st.per_call)), 4),
+                                               round(float(np.min(st.per_call)), 4)]
+                                     for st in stages},
+             "setup_s": round(setup_s, 1),
              "wall_ms_per_step": round(wall * 1e3 / args.steps, 3),
              "stages_timed_per_call_with_cache_flush": [st.name for st in stages
                                                         if getattr(st, "flushed", False)]}
