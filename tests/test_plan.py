@@ -144,6 +144,47 @@ def test_decode_plans_are_valid(checker):
     assert 0 in folds and 1 in folds  # both merge modes are exercised
 
 
+def _decode_items(kv, hkv, c):
+    return int(np.sum(-(-np.asarray(kv, dtype=np.int64) // c))) * hkv
+
+
+def _expected_auto_chunk(kv, hkv):
+    """The automatic decode chunk restated: for R rounds of 2048 waves, the shortest chunk
+    (a multiple of 32 in [512, 16384]) whose items fit, scored R * (1200 + chunk); if the
+    best leaves fewer than 4 chunks per (task, kv head), sum(kv) * Hkv / 4096 instead."""
+    best, best_score = 16384, None
+    r = max(1, -(-_decode_items(kv, hkv, 16384) // 2048))
+    while True:
+        if best_score is not None and r * (1200 + 512) >= best_score:
+            break
+        c = next(c for c in range(512, 16385, 32) if _decode_items(kv, hkv, c) <= 2048 * r)
+        if best_score is None or r * (1200 + c) < best_score:
+            best, best_score = c, r * (1200 + c)
+        if c == 512:
+            break
+        r += 1
+    if _decode_items(kv, hkv, best) < 4 * len(kv) * hkv:
+        c = -(-int(np.sum(kv)) * hkv // 4096)
+        best = min(max(-(-c // 32) * 32, 512), 16384)
+    return best
+
+
+def test_decode_auto_chunk_rule(checker):
+    """The planner's automatic decode chunk is the round rule (or, with fewer than 4 chunks
+    per unit, the item-count rule), on the bench workloads' shapes and random ones."""
+    rng = np.random.default_rng(11)
+    cases = []
+    for hq, hkv, n, lo, hi in [(28, 4, 64, 2048, 16384), (32, 8, 256, 1024, 32768),
+                               (64, 8, 32, 33000, 99000), (32, 8, 32, 5000, 28000),
+                               (28, 4, 16, 2000, 16000), (32, 8, 512, 256, 4000),
+                               (16, 2, 200, 800, 12000), (64, 8, 8, 30000, 120000),
+                               (28, 4, 1, 10, 100), (32, 8, 2048, 100, 400)]:
+        cases.append((hq, hkv, rng.integers(lo, hi, size=n)))
+    out = _run(checker, [_decode_line(hq, hkv, 128, kv) for hq, hkv, kv in cases])
+    for (hq, hkv, kv), o in zip(cases, out):
+        assert int(o[2]) == _expected_auto_chunk(kv, hkv), (hq, hkv, len(kv))
+
+
 def test_shared_decode_plans_are_valid(checker):
     """Shared-prefix decode work lists: per task and kv head the prompt chunks of its
     group and its own chunks give each split id once and tile [0, kv) in order; prompt
