@@ -297,6 +297,18 @@ def cpu_baseline_decode(wl, budget_s: float, steps: int = 1):
     return info
 
 
+def extend_vs_prefill(wl, keep, torch):
+    """Every extend row against the same row of the full re-prefill, both from the GPU at
+    full size (resume and recompute must agree): the largest and mean absolute difference."""
+    full_start = np.concatenate([[0], np.cumsum(wl.seq_lens)[:-1]])
+    rows = np.concatenate([np.arange(fs + p, fs + p + e) for fs, p, e in
+                           zip(full_start, wl.prefix_lens, wl.extend_lens)]).astype(np.int64)
+    sel = keep["out_full"][torch.from_numpy(rows).to(keep["out_full"].device)]
+    diff = (sel.float() - keep["out_ext"].float()).abs()
+    return {"rows": int(rows.size), "max_abs_diff": float(diff.max().item()),
+            "mean_abs_diff": float(diff.mean().item())}
+
+
 class Stage:
     """One timed call of the step: a callable plus its algorithmic work.  in_step=False
     marks a comparison (the same work done another way), timed on its own but not part of
@@ -341,6 +353,7 @@ def build_stages(wl, kv, dev, args, torch, np_up):
             k_full, v_full = np_up(wl.packed("k", wl.full_ranges())), np_up(wl.packed("v", wl.full_ranges()))
             q_full = np_up(wl.packed("q", wl.full_ranges()))
             out_full = torch.empty_like(q_full)
+            keep.update(out_full=out_full)
             stages.append(Stage("append_history", lambda: kv.append(k_full, v_full, zeros, wl.seq_lens),
                                 bytes_=append_bytes(wl, int(wl.seq_lens.sum()))))
             stages.append(Stage("prefill", lambda: kv.prefill(q_full, wl.seq_lens, out=out_full),
@@ -733,6 +746,7 @@ def main():
             "speedup_vs_reprefill_attention_only": round(ms["prefill"] / ms["extend"], 3),
             "flop_ratio_prefill_over_extend": round(prefill_flops(wl) / extend_flops(wl), 3),
             "prefill_tokens_per_s": round(float(wl.seq_lens.sum()) / (ms["prefill"] * 1e-3), 1),
+            "extend_vs_prefill_rows": extend_vs_prefill(wl, keep, torch),
         })
     if "fused_append_decode" in ms:
         extra["speedup_fused_vs_append_then_decode"] = round(
