@@ -50,38 +50,56 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 constexpr int64_t kDecodeWaveSlots = 2048;
 constexpr int64_t kDecodeRoundCost = 1200;  // keys
 constexpr int64_t kDecodeMinUnitChunks = 4;
+constexpr int64_t kDecodeMaxRoundsTried = 8;
 constexpr int64_t kDecodeMinChunk = 512;
 constexpr int64_t kDecodeMaxChunk = 16384;
 constexpr int64_t kDecodeTargetItems = 4096;
 constexpr int64_t kFoldMeanSplits = 4;  // merge inside the split kernel up to this mean
 
-// Items of a decode call cut into chunks of c keys: Hkv * sum over tasks of ceil(kv / c)
-// (a task's kv is its prefix + 1).
-int64_t decode_items(const std::vector<TaskDesc>& tasks, int32_t hkv, int64_t c) {
-  int64_t n = 0;
-  for (const TaskDesc& t : tasks) n += ceil_div((int64_t)t.prefix + 1, c);
-  return n * hkv;
-}
-
-// The automatic decode chunk (see kDecodeRoundCost): for R = 1, 2, ... rounds, the
-// shortest chunk (a multiple of the kernel step) whose items fit in R * 2048 waves, scored
-// R * (kDecodeRoundCost + chunk).  Items fall as the chunk grows, so each R is a binary
-// search; R stops growing once the shortest allowed chunk fits, or once R rounds of the
-// shortest chunk already score worse than the best found.
+// The automatic decode chunk (see kDecodeRoundCost).  Round rule: for R rounds from the
+// fewest that can hold the items, the shortest chunk (a multiple of the kernel step) whose
+// items fit in R * 2048 waves, scored R * (kDecodeRoundCost + chunk); items fall as the
+// chunk grows, so each R is a binary search.  R stops growing once the shortest allowed
+// chunk fits, once R rounds of it already score worse than the best found, or after
+// kDecodeMaxRoundsTried values (a few dozen passes over the tasks per call).  Item rule,
+// when the round rule would leave fewer than 4 chunks per unit (or cannot reach 4 at
+// all): sum(kv) * Hkv / 4096 keys.
 int64_t decode_auto_chunk(const std::vector<TaskDesc>& tasks, int32_t hkv) {
+  const int64_t units = (int64_t)tasks.size() * hkv;
+  // Items for a chunk of m kernel steps: Hkv * sum over tasks of ceil(kv / (32 m)), from
+  // each task's length in steps (32-bit divisions: this runs a few dozen times per call).
+  std::vector<uint32_t> steps(tasks.size());
+  for (size_t b = 0; b < tasks.size(); ++b)
+    steps[b] = (uint32_t)ceil_div((int64_t)tasks[b].prefix + 1, kDecodeStep);
+  auto items_at = [&](int64_t m) {
+    int64_t n = 0;
+    for (uint32_t k : steps) n += (k + (uint32_t)m - 1) / (uint32_t)m;
+    return n * hkv;
+  };
+  auto item_rule = [&]() {
+    int64_t total = 0;
+    for (const TaskDesc& t : tasks) total += (int64_t)t.prefix + 1;
+    int64_t c = ceil_div(total * hkv, kDecodeTargetItems);
+    c = ceil_div(c, kDecodeStep) * kDecodeStep;
+    return std::min<int64_t>(std::max<int64_t>(c, kDecodeMinChunk), kDecodeMaxChunk);
+  };
+  if (items_at(kDecodeMinChunk / kDecodeStep) < kDecodeMinUnitChunks * units) return item_rule();
   const int64_t lo_step = kDecodeMinChunk / kDecodeStep, hi_step = kDecodeMaxChunk / kDecodeStep;
-  const int64_t n_hi = decode_items(tasks, hkv, kDecodeMaxChunk);
+  const int64_t r0 = std::max<int64_t>(1, ceil_div(items_at(kDecodeMaxChunk / kDecodeStep),
+                                                   kDecodeWaveSlots));
   int64_t best = kDecodeMaxChunk, best_score = INT64_MAX;
-  for (int64_t r = std::max<int64_t>(1, ceil_div(n_hi, kDecodeWaveSlots));; ++r) {
+  int64_t hi_prev = hi_step;  // R rounds' chunk also fits R + 1 rounds: the next search's top
+  for (int64_t r = r0; r < r0 + kDecodeMaxRoundsTried; ++r) {
     if (r * (kDecodeRoundCost + kDecodeMinChunk) >= best_score) break;  // cannot win
     const int64_t cap = r * kDecodeWaveSlots;
-    int64_t lo = lo_step, hi = hi_step;  // in kernel steps; decode_items(hi) <= cap
-    if (decode_items(tasks, hkv, lo * kDecodeStep) <= cap) hi = lo;
+    int64_t lo = lo_step, hi = hi_prev;  // in kernel steps; items_at(hi) <= cap
+    if (items_at(lo) <= cap) hi = lo;
     while (hi - lo > 1) {
       const int64_t mid = (lo + hi) / 2;
-      if (decode_items(tasks, hkv, mid * kDecodeStep) <= cap) hi = mid;
+      if (items_at(mid) <= cap) hi = mid;
       else lo = mid;
     }
+    hi_prev = hi;
     const int64_t c = hi * kDecodeStep;
     const int64_t score = r * (kDecodeRoundCost + c);
     if (score < best_score) {
@@ -90,6 +108,7 @@ int64_t decode_auto_chunk(const std::vector<TaskDesc>& tasks, int32_t hkv) {
     }
     if (hi == lo_step) break;  // more rounds can only add cost
   }
+  if (items_at(best / kDecodeStep) < kDecodeMinUnitChunks * units) return item_rule();
   return best;
 }
 
@@ -480,15 +499,6 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
       chunk = std::max<int64_t>(kDecodeStep, ceil_div(chunk, kDecodeStep) * kDecodeStep);
     } else {
       chunk = decode_auto_chunk(tasks, dims.num_kv_heads);
-      if (decode_items(tasks, dims.num_kv_heads, chunk) <
-          kDecodeMinUnitChunks * (int64_t)num_tasks * dims.num_kv_heads) {
-        int64_t total = 0;
-        for (int32_t b = 0; b < num_tasks; ++b) total += (int64_t)tasks[b].prefix + 1;
-        total *= dims.num_kv_heads;
-        chunk = ceil_div(total, kDecodeTargetItems);
-        chunk = ceil_div(chunk, kDecodeStep) * kDecodeStep;
-        chunk = std::min<int64_t>(std::max<int64_t>(chunk, kDecodeMinChunk), kDecodeMaxChunk);
-      }
     }
     int32_t max_splits = 0;
     std::vector<DecodeItem> items;

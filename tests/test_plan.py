@@ -149,12 +149,21 @@ def _decode_items(kv, hkv, c):
 
 
 def _expected_auto_chunk(kv, hkv):
-    """The automatic decode chunk restated: for R rounds of 2048 waves, the shortest chunk
-    (a multiple of 32 in [512, 16384]) whose items fit, scored R * (1200 + chunk); if the
-    best leaves fewer than 4 chunks per (task, kv head), sum(kv) * Hkv / 4096 instead."""
+    """The automatic decode chunk restated: for R rounds of 2048 waves (at most 8 values of
+    R), the shortest chunk (a multiple of 32 in [512, 16384]) whose items fit, scored
+    R * (1200 + chunk); if the best leaves fewer than 4 chunks per (task, kv head), or the
+    shortest chunk already does, sum(kv) * Hkv / 4096 instead."""
+    units = len(kv) * hkv
+
+    def item_rule():
+        c = -(-int(np.sum(kv)) * hkv // 4096)
+        return min(max(-(-c // 32) * 32, 512), 16384)
+
+    if _decode_items(kv, hkv, 512) < 4 * units:
+        return item_rule()
     best, best_score = 16384, None
-    r = max(1, -(-_decode_items(kv, hkv, 16384) // 2048))
-    while True:
+    r0 = max(1, -(-_decode_items(kv, hkv, 16384) // 2048))
+    for r in range(r0, r0 + 8):
         if best_score is not None and r * (1200 + 512) >= best_score:
             break
         c = next(c for c in range(512, 16385, 32) if _decode_items(kv, hkv, c) <= 2048 * r)
@@ -162,11 +171,7 @@ def _expected_auto_chunk(kv, hkv):
             best, best_score = c, r * (1200 + c)
         if c == 512:
             break
-        r += 1
-    if _decode_items(kv, hkv, best) < 4 * len(kv) * hkv:
-        c = -(-int(np.sum(kv)) * hkv // 4096)
-        best = min(max(-(-c // 32) * 32, 512), 16384)
-    return best
+    return item_rule() if _decode_items(kv, hkv, best) < 4 * units else best
 
 
 def test_decode_auto_chunk_rule(checker):
@@ -178,7 +183,8 @@ def test_decode_auto_chunk_rule(checker):
                                (64, 8, 32, 33000, 99000), (32, 8, 32, 5000, 28000),
                                (28, 4, 16, 2000, 16000), (32, 8, 512, 256, 4000),
                                (16, 2, 200, 800, 12000), (64, 8, 8, 30000, 120000),
-                               (28, 4, 1, 10, 100), (32, 8, 2048, 100, 400)]:
+                               (28, 4, 1, 10, 100), (32, 8, 2048, 100, 400),
+                               (32, 8, 20000, 1000, 9000)]:
         cases.append((hq, hkv, rng.integers(lo, hi, size=n)))
     out = _run(checker, [_decode_line(hq, hkv, 128, kv) for hq, hkv, kv in cases])
     for (hq, hkv, kv), o in zip(cases, out):
