@@ -238,16 +238,21 @@ void extend_attn_kernel(ExtendArgs a) {
     v_src[i] = (uint32_t)(rp * S::kRowBytes + (p ^ (vseg<D>(r) << 2)) * 16);
   }
   const int lds_row0 = 8 * wave * S::kRowBytes;  // where those rows land in a tile
-  bool bad_page = false;
-  // Page id of this wave's page of local tile t (a scalar load), or kPastEnd for a page
-  // past the sequence or a tile past the item (a value no page id can take).
-  constexpr int64_t kPastEnd = -(int64_t(1) << 40);
-  auto page_word = [&](int t) -> int64_t {
-    const int lp = (tbase + t) * 4 + pw;
-    return (t < ntiles && lp < npages) ? (int64_t)load_page_id(bt, lp) : kPastEnd;
+  bool bad_page = false;  // an invalid page id met by a lane of the fused append's pool writes
+  uint32_t bad_tile = 0;  // the same for whole-wave page loads, kept in scalar registers
+  // This wave's page of local tile t: whether it is live (inside the item and the
+  // sequence) and, if so, its page id (a scalar load); ids are checked as 32-bit unsigned
+  // scalars, so a negative id compares as too large.
+  struct PageRef {
+    bool live;
+    uint32_t word;
+  };
+  auto page_ref = [&](int t) -> PageRef {
+    const bool live = t < ntiles && (tbase + t) * 4 + pw < npages;  // kNone is never live
+    return PageRef{live, live ? (uint32_t)load_page_id(bt, (tbase + t) * 4 + pw) : 0u};
   };
   // Streams this wave's rows of K tile tk into kbuf and of V tile tv into vbuf (either
-  // may be a dummy with kPastEnd).  A page past the sequence, a tile past the item and an
+  // may be kNone, a load of nothing).  A page past the sequence, a tile past the item and an
   // invalid page id are read through a zero-length buffer: zeros, no memory access.
   // With a fused append (a.k_new), a tile that holds keys at or past the prefix P takes
   // each lane's row from its source: the pool page for keys below P, the new rows for
@@ -257,11 +262,12 @@ void extend_attn_kernel(ExtendArgs a) {
   constexpr bool fused = kAppend;
   constexpr int kNone = 1 << 30;  // tile index of a load of nothing
   const int64_t new_row0 = (int64_t)td.row_start * a.num_kv_heads + it.kv_head;  // row P, this head
-  auto one_fused = [&](int t, int64_t word, const uint8_t* pool, const uint16_t* rows,
+  auto one_fused = [&](int t, PageRef pg, const uint8_t* pool, const uint16_t* rows,
                        bool is_v, uint8_t* buf) {
-    const bool past = word == kPastEnd;
-    const bool bad = !past && (word < 0 || word >= a.num_pages);
-    bad_page |= bad;
+    const bool past = !pg.live;
+    const bool bad = !past && pg.word >= (uint32_t)a.num_pages;
+    const int64_t word = pg.word;
+    bad_tile |= (uint32_t)bad;
     const int64_t blk = ((past || bad ? 0 : word) * a.num_kv_heads + it.kv_head) *
                         (int64_t)(kPage * S::kRowBytes);
 #pragma unroll
@@ -302,15 +308,14 @@ void extend_attn_kernel(ExtendArgs a) {
   // The V tile's loads go first: a wait can then cover a group's V tile without its K tile.
   // tk / tv: the local tiles loaded (only used by the fused path).  With fuse_tag false the
   // caller guarantees that both tiles lie below the prefix, and no fused code is emitted.
-  auto stream = [&](int64_t kword, uint8_t* kbuf, int64_t vword, uint8_t* vbuf, int tk, int tv,
-                    auto fuse_tag) {
+  auto stream = [&](uint8_t* kbuf, uint8_t* vbuf, int tk, int tv, auto fuse_tag) {
     constexpr bool kFuse = kAppend && decltype(fuse_tag)::value;
-    auto one = [&](int64_t word, const uint8_t* pool, const uint32_t(&src)[S::kDma], uint8_t* buf) {
-      const bool past = word == kPastEnd;
-      const bool bad = !past && (word < 0 || word >= a.num_pages);
-      bad_page |= bad;
-      const bool use = !past && !bad;
-      const int64_t blk = ((use ? word : 0) * a.num_kv_heads + it.kv_head) *
+    const PageRef kpg = page_ref(tk), vpg = page_ref(tv);
+    auto one = [&](PageRef pg, const uint8_t* pool, const uint32_t(&src)[S::kDma], uint8_t* buf) {
+      const bool ok = pg.word < (uint32_t)a.num_pages;
+      bad_tile |= (uint32_t)(pg.live && !ok);
+      const bool use = pg.live && ok;
+      const int64_t blk = ((use ? (int64_t)pg.word : 0) * a.num_kv_heads + it.kv_head) *
                           (int64_t)(kPage * S::kRowBytes);
       const int bytes = use ? kPage * S::kRowBytes : 0;
 #pragma unroll
@@ -320,15 +325,15 @@ void extend_attn_kernel(ExtendArgs a) {
     // wholly at or past P reads the new rows, the one holding key P mixes both sources
     if (kFuse && tv < ntiles && (tbase + tv + 1) * 64 > P) {
       if ((tbase + tv) * 64 >= P) one_new(tv, a.v_new, true, vbuf);
-      else one_fused(tv, vword, vpool, a.v_new, true, vbuf);
+      else one_fused(tv, vpg, vpool, a.v_new, true, vbuf);
     } else {
-      one(vword, vpool, v_src, vbuf);
+      one(vpg, vpool, v_src, vbuf);
     }
     if (kFuse && tk < ntiles && (tbase + tk + 1) * 64 > P) {
       if ((tbase + tk) * 64 >= P) one_new(tk, a.k_new, false, kbuf);
-      else one_fused(tk, kword, kpool, a.k_new, false, kbuf);
+      else one_fused(tk, kpg, kpool, a.k_new, false, kbuf);
     } else {
-      one(kword, kpool, k_src, kbuf);
+      one(kpg, kpool, k_src, kbuf);
     }
   };
   const std::true_type fuse;  // streams that may cross the prefix (fused variant only)
@@ -353,13 +358,13 @@ void extend_attn_kernel(ExtendArgs a) {
   // its P.V product, in V(t), before that barrier.  The prologue issues the earlier
   // tiles in groups of the same shape (the first two with a V load of nothing), so one
   // wait count serves everywhere.
-  stream(page_word(0), k_lds0, kPastEnd, v_lds2, 0, kNone, fuse);  // K(0)
+  stream(k_lds0, v_lds2, 0, kNone, fuse);  // K(0)
   __builtin_amdgcn_sched_barrier(0);               // keep the issue order the waits count on
-  stream(page_word(1), k_lds1, kPastEnd, v_lds3, 1, kNone, fuse);  // K(1)
+  stream(k_lds1, v_lds3, 1, kNone, fuse);  // K(1)
   __builtin_amdgcn_sched_barrier(0);
-  stream(page_word(2), k_lds2, page_word(0), v_lds0, 2, 0, fuse);  // V(0), K(2)
+  stream(k_lds2, v_lds0, 2, 0, fuse);  // V(0), K(2)
   __builtin_amdgcn_sched_barrier(0);
-  stream(page_word(3), k_lds3, page_word(1), v_lds1, 3, 1, fuse);  // V(1), K(3)
+  stream(k_lds3, v_lds1, 3, 1, fuse);  // V(1), K(3)
   wait_vmem<3 * S::kGroup>();  // the query rows and K(0) landed
   tile_barrier();
 
@@ -512,7 +517,8 @@ void extend_attn_kernel(ExtendArgs a) {
     float mc[4], mt = 0.0f, m_new = 0.0f, alpha = 1.0f, negm = 0.0f;
     float x[32], pr[32];
     uint32_t w[16];
-    float lt[4] = {0.0f, 0.0f, 0.0f, 0.0f}, le[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    // row sums of the tile: two chains, the first continuing the rescaled running sum
+    float lt[2], le[2];
     auto E = [&](int f) -> float { return s[f >> 4][f & 15]; };
     // vector op k of the softmax
     auto op = [&](auto k_tag) {
@@ -532,7 +538,9 @@ void extend_attn_kernel(ExtendArgs a) {
       } else if constexpr (k - nMask == 17) {
         mt = max3(mt, mc[3], mc[3]);
       } else if constexpr (k - nMask == 18) {
-        mt = pair_max(mt);
+        float x0, x1;
+        lane_pair(mt, x0, x1);
+        mt = max3(x0, x1, x1);
       } else if constexpr (k - nMask == 19) {
         mt *= csc;
       } else if constexpr (k - nMask == 20) {
@@ -557,14 +565,18 @@ void extend_attn_kernel(ExtendArgs a) {
           asm volatile("" ::"v"(w[i]));
         } else if constexpr (r < 12) {
           constexpr int i = 2 * g + r - 10;
-          lt[i % 4] = add_bf16x2(w[i], lt[i % 4]);
+          if constexpr (i == 0) lt[0] = add_bf16x2(w[0], l_part * alpha);
+          else if constexpr (i == 1) lt[1] = add_bf16x2(w[1], 0.0f);
+          else lt[i % 2] = add_bf16x2(w[i], lt[i % 2]);
         } else {
           constexpr int i = 2 * g + r - 12;
-          le[i % 4] += pr[2 * i] + pr[2 * i + 1];
+          if constexpr (i == 0) le[0] = fmaf(l_exact, alpha, pr[0] + pr[1]);
+          else if constexpr (i == 1) le[1] = pr[2] + pr[3];
+          else le[i % 2] += pr[2 * i] + pr[2 * i + 1];
         }
       } else {
-        l_part = fmaf(l_part, alpha, (lt[0] + lt[1]) + (lt[2] + lt[3]));
-        if constexpr (kLse) l_exact = fmaf(l_exact, alpha, (le[0] + le[1]) + (le[2] + le[3]));
+        l_part = lt[0] + lt[1];
+        if constexpr (kLse) l_exact = le[0] + le[1];
         asm volatile("" ::"v"(l_part));
       }
     };
@@ -585,7 +597,7 @@ void extend_attn_kernel(ExtendArgs a) {
   qk(k_lds0, sa);
   wait_vmem<S::kGroup + S::kDma>();  // V(0) and K(1) landed
   tile_barrier();
-  stream(page_word(4), k_lds0, page_word(2), v_lds2, 4, 2, fuse);
+  stream(k_lds0, v_lds2, 4, 2, fuse);
 
   // ---- iteration 0: softmax(0) with S(1) ---------------------------------------------
   u32x4 pre_a[kAhead], pre_b[kAhead];  // first operands of odd / even iterations
@@ -601,7 +613,7 @@ void extend_attn_kernel(ExtendArgs a) {
   }
   wait_vmem<S::kGroup + S::kDma>();  // V(1) and K(2) landed
   tile_barrier();
-  stream(page_word(5), k_lds1, page_word(3), v_lds3, 5, 3, fuse);
+  stream(k_lds1, v_lds3, 5, 3, fuse);
 
   // ---- iteration i >= 1: softmax(i) with P.V(i-1) and S(i+1) ----------------------------
   // Slots are fixed by i mod 4: S(i+1) reads K slot (i+1) mod 4, P.V(i-1) reads V slot
@@ -616,7 +628,7 @@ void extend_attn_kernel(ExtendArgs a) {
                   vb_next, pre_next));
     wait_vmem<S::kGroup + S::kDma>();  // V(i+1) and K(i+2) landed
     tile_barrier();
-    stream(page_word(i + 5), kb, page_word(i + 3), vb, i + 5, i + 3, fuse_tag);
+    stream(kb, vb, i + 5, i + 3, fuse_tag);
   };
   auto four = [&](auto diag_tag, auto fuse_tag, int i) __attribute__((always_inline)) {
     step(diag_tag, fuse_tag, i, k_lds2, v_lds0, v_lds1, sb, sa, pa, pb, pre_a, pre_b);
@@ -688,9 +700,10 @@ void extend_attn_kernel(ExtendArgs a) {
   }
 
   if constexpr (kAppend) {  // the pool writes test page ids per lane
-    if (__builtin_amdgcn_ballot_w64(bad_page) != 0 && lane == 0) atomicOr(a.error_flags, 1);
+    if ((__builtin_amdgcn_ballot_w64(bad_page) != 0 || bad_tile) && lane == 0)
+      atomicOr(a.error_flags, 1);
   } else {
-    if (bad_page && lane == 0) atomicOr(a.error_flags, 1);
+    if (bad_tile && lane == 0) atomicOr(a.error_flags, 1);
   }
   const float l_tot = pair_sum(l_part);
   if (kSplit && split >= 0) {
