@@ -556,28 +556,37 @@ void extend_attn_kernel(ExtendArgs a) {
           x[4 * g + r] = fmaf(E(4 * g + r), csc, negm);
         } else if constexpr (r < 8) {
           pr[4 * g + r - 4] = fast_exp2(x[4 * g + r - 4]);
-        } else if constexpr (r < 10) {
-          constexpr int i = 2 * g + r - 8;
-          w[i] = pack_bf16x2(pr[2 * i], pr[2 * i + 1]);
-          pcur[i / 4][i % 4] = w[i];
-          // keeps the word (and the FMAs and exponentials behind it) in this slot: the
-          // compiler would otherwise sink them to where the next step first reads them
-          asm volatile("" ::"v"(w[i]));
-        } else if constexpr (r < 12) {
-          constexpr int i = 2 * g + r - 10;
-          if constexpr (i == 0) lt[0] = add_bf16x2(w[0], l_part * alpha);
-          else if constexpr (i == 1) lt[1] = add_bf16x2(w[1], 0.0f);
-          else lt[i % 2] = add_bf16x2(w[i], lt[i % 2]);
         } else {
-          constexpr int i = 2 * g + r - 12;
-          if constexpr (i == 0) le[0] = fmaf(l_exact, alpha, pr[0] + pr[1]);
-          else if constexpr (i == 1) le[1] = pr[2] + pr[3];
-          else le[i % 2] += pr[2 * i] + pr[2 * i + 1];
+          // then per word i = 2g, 2g+1: the bf16 pack, with kLse at once the exact fp32 sum
+          // of its two probabilities (so they die here), and the rounded-weight row sums
+          constexpr int rr = r - 8;
+          constexpr int kind = kLse ? (rr < 4 ? rr % 2 : 2) : (rr < 2 ? 0 : 2);  // pack, exact, sum
+          constexpr int i = 2 * g + (kLse ? (rr < 4 ? rr / 2 : rr - 4) : rr % 2);
+          if constexpr (kind == 0) {
+            w[i] = pack_bf16x2(pr[2 * i], pr[2 * i + 1]);
+            pcur[i / 4][i % 4] = w[i];
+            // keeps the word (and the FMAs and exponentials behind it) in this slot: the
+            // compiler would otherwise sink them to where the next step first reads them
+            asm volatile("" ::"v"(w[i]));
+          } else if constexpr (kind == 1) {
+            if constexpr (i == 0) le[0] = fmaf(l_exact, alpha, pr[0] + pr[1]);
+            else if constexpr (i == 1) le[1] = pr[2] + pr[3];
+            else le[i % 2] += pr[2 * i] + pr[2 * i + 1];
+          } else {
+            if constexpr (i == 0) lt[0] = add_bf16x2(w[0], l_part * alpha);
+            else if constexpr (i == 1) lt[1] = add_bf16x2(w[1], 0.0f);
+            else lt[i % 2] = add_bf16x2(w[i], lt[i % 2]);
+          }
         }
       } else {
         l_part = lt[0] + lt[1];
-        if constexpr (kLse) l_exact = le[0] + le[1];
         asm volatile("" ::"v"(l_part));
+        if constexpr (kLse) {
+          l_exact = le[0] + le[1];
+          // like the words above: without it the exact sums (and every probability they
+          // read) would be sunk into the next step, where l_exact is next used
+          asm volatile("" ::"v"(l_exact));
+        }
       }
     };
 
