@@ -262,6 +262,7 @@ void extend_attn_kernel(ExtendArgs a) {
   constexpr bool fused = kAppend;
   constexpr int kNone = 1 << 30;  // tile index of a load of nothing
   const int64_t new_row0 = (int64_t)td.row_start * a.num_kv_heads + it.kv_head;  // row P, this head
+  const uint32_t new_stride_b = (uint32_t)a.num_kv_heads * S::kRowBytes;  // bytes per token row
   auto one_fused = [&](int t, PageRef pg, const uint8_t* pool, const uint16_t* rows,
                        bool is_v, uint8_t* buf) {
     const bool past = !pg.live;
@@ -270,20 +271,29 @@ void extend_attn_kernel(ExtendArgs a) {
     bad_tile |= (uint32_t)bad;
     const int64_t blk = ((past || bad ? 0 : word) * a.num_kv_heads + it.kv_head) *
                         (int64_t)(kPage * S::kRowBytes);
+    // Each lane's address is a wave-uniform base (the new rows of this kv head, or the
+    // pool page) plus a 32-bit lane offset.  The offset passes through an empty asm so
+    // that the compiler cannot hoist per-lane 64-bit addresses out of the walk: kept live
+    // across it they were spilled, and every reload drained the prefetch queue.
+    const uint8_t* new_base = reinterpret_cast<const uint8_t*>(rows + new_row0 * D);
+    const uint8_t* page_base = pool + blk;
+    int ln = lane;  // lane constants too are recomputed here rather than kept live
+    asm volatile("" : "+v"(ln));
 #pragma unroll
     for (int i = 0; i < S::kDma; ++i) {
-      const int r = 8 * wave + i * S::kRowsPerDma + lane / S::kNG;  // tile row
-      const int p = lane % S::kNG;
+      const int r = 8 * wave + i * S::kRowsPerDma + ln / S::kNG;  // tile row
+      const int p = ln % S::kNG;
       const int g = is_v ? (p ^ (vseg<D>(r) << 2)) : kswz<D>(r, p);  // logical granule
       const int key = (tbase + t) * 64 + r;
-      const uint8_t* src;
-      if (key >= P && key < seq_len)
-        src = reinterpret_cast<const uint8_t*>(rows + (new_row0 + (int64_t)(key - P) * a.num_kv_heads) * D) + 16 * g;
-      else if (key < P && !past && !bad)
-        src = pool + blk + (r % kPage) * S::kRowBytes + 16 * g;
-      else
-        src = reinterpret_cast<const uint8_t*>(rows + new_row0 * D);
-      dma16_lane(src, buf + lds_row0 + i * 1024);
+      const bool is_new = key >= P && key < seq_len;
+      const bool is_old = key < P && !past && !bad;
+      // both offsets computed and masked (is_new and is_old exclude each other), so the
+      // choice is a select rather than a divergent branch
+      const uint32_t off_new = (uint32_t)(key - P) * new_stride_b + 16u * g;
+      const uint32_t off_old = (uint32_t)((r % kPage) * S::kRowBytes + 16 * g);
+      uint32_t off = (off_new & (0u - (uint32_t)is_new)) | (off_old & (0u - (uint32_t)is_old));
+      asm volatile("" : "+v"(off));
+      dma16_lane((is_old ? page_base : new_base) + off, buf + lds_row0 + i * 1024);
     }
   };
   // A tile whose keys all lie at or past P (and below seq_len, or zero-filled past it) is
