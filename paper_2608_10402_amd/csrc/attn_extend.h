@@ -612,6 +612,30 @@ void extend_attn_kernel(ExtendArgs a) {
     return alpha;
   };
 
+  // A wave whose 32 rows all lie past the block's tokens (the last, partial block of a
+  // task) has nothing to compute: it only streams its rows of every K and V tile and
+  // meets the workgroup at every barrier, in the same order as the computing waves (one
+  // barrier after iteration -1, one after iteration 0 and one after each iteration
+  // 1 .. ntiles - 1, each followed by the same group of loads into the same slots).
+  // Its SIMD partner then runs alone.
+  const bool wave_idle = wave * 32 >= it.ntok * G;
+  if (wave_idle) {
+    wait_vmem<S::kGroup + S::kDma>();
+    tile_barrier();
+    stream(k_lds0, v_lds2, 4, 2, fuse);
+    wait_vmem<S::kGroup + S::kDma>();
+    tile_barrier();
+    stream(k_lds1, v_lds3, 5, 3, fuse);
+    for (int i = 1; i < ntiles; ++i) {
+      wait_vmem<S::kGroup + S::kDma>();
+      tile_barrier();
+      const int ks = (i + 1) & 3, vs = (i + 3) & 3;
+      stream(ks == 0 ? k_lds0 : ks == 1 ? k_lds1 : ks == 2 ? k_lds2 : k_lds3,
+             vs == 0 ? v_lds0 : vs == 1 ? v_lds1 : vs == 2 ? v_lds2 : v_lds3, i + 5, i + 3, fuse);
+    }
+    wait_vmem<0>();  // no transfer into LDS may outlive the workgroup
+  } else {
+
   // ---- iteration -1: S(0), then K(4) / V(2) into the slots it leaves free ------------
   qk(k_lds0, sa);
   wait_vmem<S::kGroup + S::kDma>();  // V(0) and K(1) landed
@@ -695,6 +719,7 @@ void extend_attn_kernel(ExtendArgs a) {
     default: pv_tail(v_lds3, pb, last); break;
   }
   wait_vmem<0>();  // no transfer into LDS may outlive the workgroup
+  }  // computing waves
 
   // Fused append: this item's tokens' K/V rows into their pool slots (one chunk per item
   // writes).  No workgroup of this call reads those slots -- keys at or past P come from
