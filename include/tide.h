@@ -53,8 +53,8 @@
  *   stream           a hipStream_t passed as void*; NULL means the default stream.
  *
  * Supported shapes: head_dim in {64, 128}; page_size == 16; num_q_heads a multiple of
- * num_kv_heads with G = num_q_heads / num_kv_heads in [1, 16].  Anything else returns
- * TIDE_ERR_UNSUPPORTED.
+ * num_kv_heads with G = num_q_heads / num_kv_heads in [1, 16]; num_kv_heads <= 65536.
+ * Anything else returns TIDE_ERR_UNSUPPORTED.
  *
  * Semantics guaranteed by every attention entry point:
  *   - Pool slots at or beyond a task's current length, and pages not listed in its

@@ -228,6 +228,10 @@ void extend_attn_kernel(ExtendArgs a) {
   const uint8_t* kpool = reinterpret_cast<const uint8_t*>(a.k_pool);
   const uint8_t* vpool = reinterpret_cast<const uint8_t*>(a.v_pool);
   const int pw = wave >> 1;  // page of the tile these rows sit in
+  // a page of one kv head is kPage * kRowBytes bytes; a pool page holds num_kv_heads of them
+  const uint32_t page_bytes = (uint32_t)a.num_kv_heads * (kPage * S::kRowBytes);
+  const uint8_t* kpool_h = kpool + (int64_t)it.kv_head * (kPage * S::kRowBytes);
+  const uint8_t* vpool_h = vpool + (int64_t)it.kv_head * (kPage * S::kRowBytes);
   uint32_t k_src[S::kDma], v_src[S::kDma];  // this lane's byte offsets inside the page block
 #pragma unroll
   for (int i = 0; i < S::kDma; ++i) {
@@ -241,15 +245,22 @@ void extend_attn_kernel(ExtendArgs a) {
   bool bad_page = false;  // an invalid page id met by a lane of the fused append's pool writes
   uint32_t bad_tile = 0;  // the same for whole-wave page loads, kept in scalar registers
   // This wave's page of local tile t: whether it is live (inside the item and the
-  // sequence) and, if so, its page id (a scalar load); ids are checked as 32-bit unsigned
-  // scalars, so a negative id compares as too large.
+  // sequence) and its page id (a scalar load; ids are checked as 32-bit unsigned scalars,
+  // so a negative id compares as too large).  Local tiles t < t_live are live (page
+  // 4 * (tbase + t) + pw < npages); kNone never is.  The load is unconditional, of entry 0
+  // for a page that is not live (every sequence has at least one page), at a 32-bit byte
+  // offset from the row that the scalar load takes in its offset register: no branch,
+  // no 64-bit address arithmetic, and it can be issued well before the id is used.
+  const int t_live = min(ntiles, max(0, (npages - pw - 4 * tbase + 3) / 4));
+  const uint32_t pw_off = 4u * (uint32_t)(4 * tbase + pw);
   struct PageRef {
     bool live;
     uint32_t word;
   };
   auto page_ref = [&](int t) -> PageRef {
-    const bool live = t < ntiles && (tbase + t) * 4 + pw < npages;  // kNone is never live
-    return PageRef{live, live ? (uint32_t)load_page_id(bt, (tbase + t) * 4 + pw) : 0u};
+    const bool live = t < t_live;
+    const uint32_t off = live ? 16u * (uint32_t)t + pw_off : 0u;
+    return PageRef{live, (uint32_t)*(const_i32*)(reinterpret_cast<const uint8_t*>(bt) + off)};
   };
   // Streams this wave's rows of K tile tk into kbuf and of V tile tv into vbuf (either
   // may be kNone, a load of nothing).  A page past the sequence, a tile past the item and an
@@ -318,18 +329,19 @@ void extend_attn_kernel(ExtendArgs a) {
   // The V tile's loads go first: a wait can then cover a group's V tile without its K tile.
   // tk / tv: the local tiles loaded (only used by the fused path).  With fuse_tag false the
   // caller guarantees that both tiles lie below the prefix, and no fused code is emitted.
-  auto stream = [&](uint8_t* kbuf, uint8_t* vbuf, int tk, int tv, auto fuse_tag) {
+  // kpg / vpg: the pages of tk and tv, from page_ref.
+  auto stream_pages = [&](uint8_t* kbuf, uint8_t* vbuf, int tk, int tv, PageRef kpg, PageRef vpg,
+                          auto fuse_tag) {
     constexpr bool kFuse = kAppend && decltype(fuse_tag)::value;
-    const PageRef kpg = page_ref(tk), vpg = page_ref(tv);
-    auto one = [&](PageRef pg, const uint8_t* pool, const uint32_t(&src)[S::kDma], uint8_t* buf) {
+    // pool_h: the pool's block of this kv head in page 0; pages are page_bytes apart
+    auto one = [&](PageRef pg, const uint8_t* pool_h, const uint32_t(&src)[S::kDma], uint8_t* buf) {
       const bool ok = pg.word < (uint32_t)a.num_pages;
       bad_tile |= (uint32_t)(pg.live && !ok);
       const bool use = pg.live && ok;
-      const int64_t blk = ((use ? (int64_t)pg.word : 0) * a.num_kv_heads + it.kv_head) *
-                          (int64_t)(kPage * S::kRowBytes);
+      const uint8_t* base = pool_h + (uint64_t)(use ? pg.word : 0u) * page_bytes;
       const int bytes = use ? kPage * S::kRowBytes : 0;
 #pragma unroll
-      for (int i = 0; i < S::kDma; ++i) dma16(pool + blk, bytes, src[i], buf + lds_row0 + i * 1024);
+      for (int i = 0; i < S::kDma; ++i) dma16(base, bytes, src[i], buf + lds_row0 + i * 1024);
     };
     // a tile past the item keeps the zero-length path (its keys are never used); a tile
     // wholly at or past P reads the new rows, the one holding key P mixes both sources
@@ -337,14 +349,17 @@ void extend_attn_kernel(ExtendArgs a) {
       if ((tbase + tv) * 64 >= P) one_new(tv, a.v_new, true, vbuf);
       else one_fused(tv, vpg, vpool, a.v_new, true, vbuf);
     } else {
-      one(vpg, vpool, v_src, vbuf);
+      one(vpg, vpool_h, v_src, vbuf);
     }
     if (kFuse && tk < ntiles && (tbase + tk + 1) * 64 > P) {
       if ((tbase + tk) * 64 >= P) one_new(tk, a.k_new, false, kbuf);
       else one_fused(tk, kpg, kpool, a.k_new, false, kbuf);
     } else {
-      one(kpg, kpool, k_src, kbuf);
+      one(kpg, kpool_h, k_src, kbuf);
     }
+  };
+  auto stream = [&](uint8_t* kbuf, uint8_t* vbuf, int tk, int tv, auto fuse_tag) {
+    stream_pages(kbuf, vbuf, tk, tv, page_ref(tk), page_ref(tv), fuse_tag);
   };
   const std::true_type fuse;  // streams that may cross the prefix (fused variant only)
 
@@ -667,11 +682,14 @@ void extend_attn_kernel(ExtendArgs a) {
                   const uint8_t* vb_next, f32x16(&s)[2], f32x16(&sn)[2],
                   const u32x4(&pprev)[4], u32x4(&pcur)[4], const u32x4(&pre)[kAhead],
                   u32x4(&pre_next)[kAhead]) __attribute__((always_inline)) {
-    rescale(block(std::true_type(), diag_tag, tbase + i, s, pcur, pprev, vb, kb, sn, pre,
-                  vb_next, pre_next));
+    const float alpha = block(std::true_type(), diag_tag, tbase + i, s, pcur, pprev, vb, kb, sn,
+                              pre, vb_next, pre_next);
+    // the page ids of the next loads, fetched now so that the barrier hides their latency
+    const PageRef kpg = page_ref(i + 5), vpg = page_ref(i + 3);
+    rescale(alpha);
     wait_vmem<S::kGroup + S::kDma>();  // V(i+1) and K(i+2) landed
     tile_barrier();
-    stream(kb, vb, i + 5, i + 3, fuse_tag);
+    stream_pages(kb, vb, i + 5, i + 3, kpg, vpg, fuse_tag);
   };
   auto four = [&](auto diag_tag, auto fuse_tag, int i) __attribute__((always_inline)) {
     step(diag_tag, fuse_tag, i, k_lds2, v_lds0, v_lds1, sb, sa, pa, pb, pre_a, pre_b);

@@ -20,6 +20,7 @@ int check_dims(const tide_dims* dims) {
   if (dims->page_size != kPage) return TIDE_ERR_UNSUPPORTED;
   if (dims->num_q_heads % dims->num_kv_heads != 0) return TIDE_ERR_UNSUPPORTED;
   if (dims->num_q_heads / dims->num_kv_heads > kMaxGroup) return TIDE_ERR_UNSUPPORTED;
+  if (dims->num_kv_heads > kMaxKvHeads) return TIDE_ERR_UNSUPPORTED;
   return TIDE_OK;
 }
 

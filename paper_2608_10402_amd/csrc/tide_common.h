@@ -8,6 +8,9 @@ namespace tide {
 
 constexpr int kPage = 16;         // tokens per page
 constexpr int kMaxGroup = 16;     // largest supported Hq / Hkv
+// Largest supported Hkv: a pool page (Hkv blocks of kPage rows of head_dim bf16) then
+// spans at most 2^28 bytes, which the extend kernel's 32-bit page stride holds.
+constexpr int kMaxKvHeads = 65536;
 constexpr int kExtendKeyTile = 64;  // keys per extend-kernel iteration (4 pages)
 constexpr int kDecodeStep = 32;   // keys per decode-kernel iteration (2 pages)
 constexpr int kWsAlign = 256;

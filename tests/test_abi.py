@@ -74,6 +74,7 @@ GOOD = _lib.make_dims(28, 4, 128, 1 / math.sqrt(128))
     (_lib.make_dims(8, 2, 96, 0.1), tide.TIDE_ERR_UNSUPPORTED),      # head_dim 96
     (_lib.make_dims(8, 3, 64, 0.1), tide.TIDE_ERR_UNSUPPORTED),      # 8 % 3 != 0
     (_lib.make_dims(34, 2, 64, 0.1), tide.TIDE_ERR_UNSUPPORTED),     # group 17 > 16
+    (_lib.make_dims(65537, 65537, 64, 0.1), tide.TIDE_ERR_UNSUPPORTED),  # Hkv > 65536
     (_lib.make_dims(8, 2, 64, 0.1, page_size=32), tide.TIDE_ERR_UNSUPPORTED),
     (_lib.make_dims(0, 2, 64, 0.1), tide.TIDE_ERR_INVALID_ARG),
     (_lib.make_dims(8, 2, 64, 0.0), tide.TIDE_ERR_INVALID_ARG),
