@@ -192,21 +192,24 @@ __device__ __forceinline__ void merge_kv_head(const DecodeArgs& a, int task, int
   const int lane = threadIdx.x & 63;
   const int hh = lane >> 3, sub = lane & 7;
   const int G = a.group;
+  // one buffer over the group's partial rows (wave-uniform); a lane's row is its offset
+  const int64_t row0 = (int64_t)task * a.num_q_heads + kv_h * G;
+  const auto ml = __builtin_amdgcn_make_buffer_rsrc(a.part_ml + row0 * a.max_splits * 4, 0,
+                                                    G * a.max_splits * 16, 0x00020000);
+  const auto po = __builtin_amdgcn_make_buffer_rsrc(a.part_o + row0 * a.max_splits * D, 0,
+                                                    G * a.max_splits * D * 4, 0x00020000);
   for (int j0 = 0; j0 < G; j0 += 8) {
     const int j = j0 + hh;
     const bool ok = j < G;
-    const int64_t row = (int64_t)task * a.num_q_heads + kv_h * G + (ok ? j : 0);
-    const auto ml = __builtin_amdgcn_make_buffer_rsrc(a.part_ml + row * a.max_splits * 4, 0,
-                                                      a.max_splits * 16, 0x00020000);
-    const auto po = __builtin_amdgcn_make_buffer_rsrc(a.part_o + row * a.max_splits * D, 0,
-                                                      a.max_splits * D * 4, 0x00020000);
+    const int64_t row = row0 + (ok ? j : 0);
+    const int rs = (ok ? j : 0) * a.max_splits;  // the lane's first partial row
     float mx = kNoMax;
     for (int s0 = 0; s0 < n; s0 += 16) {
       float m[16];
 #pragma unroll
       for (int i = 0; i < 16; ++i)
         m[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                             ml, 16 * min(s0 + i, n - 1), 0, kDeviceScope));
+                                             ml, 16 * (rs + min(s0 + i, n - 1)), 0, kDeviceScope));
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, m[i]);  // repeats of split n-1 are harmless
     }
@@ -220,11 +223,11 @@ __device__ __forceinline__ void merge_kv_head(const DecodeArgs& a, int task, int
       for (int i = 0; i < kBatch; ++i) {
         const int sp = min(s0 + i, n - 1);  // past n: a valid slot, not summed below
         st[i] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                              ml, 16 * sp, 0, kDeviceScope));
+                                              ml, 16 * (rs + sp), 0, kDeviceScope));
 #pragma unroll
         for (int k = 0; k < kPer / 4; ++k)
           src[i][k] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                    po, 4 * (sp * D + kPer * sub + 4 * k), 0,
+                                                    po, 4 * ((rs + sp) * D + kPer * sub + 4 * k), 0,
                                                     kDeviceScope));
       }
 #pragma unroll
@@ -537,10 +540,16 @@ void decode_split_kernel(DecodeArgs a) {
         *reinterpret_cast<f32x4*>(po + 16 * t + 4 * grp) = o[t];
       if (grp == 0) *reinterpret_cast<f32x4*>(a.part_ml + slot * 4) = ml;
     } else if (a.tickets) {  // merged in this kernel, possibly by a wave on another XCD
+      // One buffer over the partial rows of this (task, kv head), the same for the whole
+      // wave, and each lane's row as its offset: a per-lane buffer base would make the
+      // compiler loop over the distinct bases around every store.
+      const int64_t row0 = ((int64_t)ctask * a.num_q_heads + kv_h * G) * a.max_splits;
+      const uint32_t r = (uint32_t)(chead * a.max_splits + split);
+      const uint32_t nrows = (uint32_t)(G * a.max_splits);
 #pragma unroll
       for (int t = 0; t < D / 16; ++t)
-        store_f32x4_device(po, D * 4, 4 * (16 * t + 4 * grp), o[t]);
-      if (grp == 0) store_f32x4_device(a.part_ml + slot * 4, 16, 0, ml);
+        store_f32x4_device(a.part_o + row0 * D, nrows * D * 4, 4 * (r * D + 16 * t + 4 * grp), o[t]);
+      if (grp == 0) store_f32x4_device(a.part_ml + row0 * 4, nrows * 16, 16 * r, ml);
     } else {  // merged by the merge kernel
 #pragma unroll
       for (int t = 0; t < D / 16; ++t)

@@ -542,7 +542,10 @@ int make_plan(int op, int32_t num_tasks, const int32_t* lens_a, const int32_t* l
     // splits on average; with many, the merge tail at the end of the launch (each merge
     // one wave, latency-bound) costs more than a merge kernel (measured on MI355X: at 2.5
     // splits per task the fold saves the merge kernel's 10 us; at 16 it adds 40-57 us).
-    plan->fold_merge = n_items <= (int64_t)kFoldMeanSplits * num_tasks * dims.num_kv_heads;
+    // (and the partial rows of one (task, kv head) must fit a 32-bit buffer range)
+    plan->fold_merge = n_items <= (int64_t)kFoldMeanSplits * num_tasks * dims.num_kv_heads &&
+                       (int64_t)(dims.num_q_heads / dims.num_kv_heads) * max_splits *
+                               dims.head_dim * 4 <= INT32_MAX;
     if (build_blob) {
       items_bytes.resize(items.size() * sizeof(DecodeItem));
       if (!items.empty()) memcpy(items_bytes.data(), items.data(), items_bytes.size());
