@@ -370,7 +370,9 @@ void decode_split_kernel(DecodeArgs a) {
   for (int t = 0; t < D / 16; ++t) o[t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   float m_ref = kNoMax, l_part = 0.0f, l_exact = 0.0f;
 
-  auto compute = [&](DecodeRegs<D>& cur, const uint8_t* kbuf, int k) {
+  // tail_tag: whether this step may hold keys at or past kend.  Only a split's last step
+  // can (every earlier step ends at or below kend), so the others skip the masks.
+  auto compute = [&](DecodeRegs<D>& cur, const uint8_t* kbuf, int k, auto tail_tag) {
     // S^T for page t: s[t][e] is key k + 16*t + 4*grp + e of query head `col`
     f32x4 s[2];
 #pragma unroll
@@ -384,7 +386,7 @@ void decode_split_kernel(DecodeArgs a) {
       }
     }
     // keys at or past kend (the context's end, or the shared prefix's) are not this item's
-    const bool tail = k + 2 * kPage > kend;
+    const bool tail = decltype(tail_tag)::value && k + 2 * kPage > kend;
     float mt = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -481,23 +483,25 @@ void decode_split_kernel(DecodeArgs a) {
     // the scheduling barriers keep each step's loads issued before the reads of the
     // step before it (which would otherwise be hoisted above them, and wait with the
     // next step not yet in flight)
+    const std::false_type inner;
+    const std::true_type last;
     load(ra, ka, kbeg, policy_tag);
     int k = kbeg;
     for (int i = 0; i + 2 < nsteps; i += 2, k += 2 * kDecodeStep) {
       load(rb, kb, k + kDecodeStep, policy_tag);
       __builtin_amdgcn_sched_barrier(0);
-      compute(ra, ka, k);
+      compute(ra, ka, k, inner);
       load(ra, ka, k + 2 * kDecodeStep, policy_tag);
       __builtin_amdgcn_sched_barrier(0);
-      compute(rb, kb, k + kDecodeStep);
+      compute(rb, kb, k + kDecodeStep, inner);
     }
     if (k + kDecodeStep < kend) {
       load(rb, kb, k + kDecodeStep, policy_tag);
       __builtin_amdgcn_sched_barrier(0);
-      compute(ra, ka, k);
-      compute(rb, kb, k + kDecodeStep);
+      compute(ra, ka, k, inner);
+      compute(rb, kb, k + kDecodeStep, last);
     } else {
-      compute(ra, ka, k);
+      compute(ra, ka, k, last);
     }
   };
   if (kShared && ntasks > 1)
