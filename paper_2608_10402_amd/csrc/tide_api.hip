@@ -5,7 +5,10 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <sched.h>
+
 #include <algorithm>
+#include <chrono>
 #include <mutex>
 #include <new>
 #include <vector>
@@ -26,22 +29,56 @@ constexpr size_t kStagingMin = 2u << 20;
 
 // Pinned, device-mapped host buffers the work lists are staged in.  A kernel on the
 // caller's stream copies a slot into the workspace (no DMA-engine copy, so no hand-off
-// between engines on every call).  A slot is reused only after the event recorded
-// behind that copy has completed, so a call never overwrites bytes a queued copy has
-// yet to read.
+// between engines on every call).  A slot is reused only once that copy has read it:
+// each of the copy's workgroups, after all its reads have returned, writes the slot's
+// use count into its own flag in coherent host memory, and the host checks the flags
+// before it overwrites the slot.  (A completion event recorded behind each copy did the
+// same, but delayed the call's next kernel by several microseconds.)
 struct StagingSlot {
   void* host = nullptr;
   const void* dev = nullptr;  // the same memory as seen from the device
   size_t cap = 0;
-  hipEvent_t done = nullptr;
+  uint32_t* flags = nullptr;  // one per copy workgroup, coherent host memory
+  uint32_t* flags_dev = nullptr;
+  uint32_t seq = 0;           // uses of the slot so far
+  uint32_t nblocks = 0;       // workgroups of the last copy
   bool pending = false;
 };
 
-// 16 bytes per thread from the staging slot (host memory) into the workspace.
+constexpr int kCopyBytesPerBlock = 256 * 16;
+
+// 16 bytes per thread from the staging slot (host memory) into the workspace; then the
+// workgroup's flag.  Every thread's load has returned once it has issued its store (the
+// store needs the data), so after the barrier the workgroup has read all it will read.
 __global__ __launch_bounds__(256) void stage_copy_kernel(u32x4_t* dst, const u32x4_t* src,
-                                                         size_t n16) {
+                                                         size_t n16, uint32_t* done, uint32_t seq) {
   const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (i < n16) dst[i] = src[i];
+  __syncthreads();
+  if (threadIdx.x == 0)
+    __hip_atomic_store(done + blockIdx.x, seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// Waits until every workgroup of the slot's last copy has set its flag.  Normally the
+// copy finished long ago; if not, this waits like a synchronisation on it would, and
+// after a few seconds falls back to a device synchronisation (which reports a failed
+// device) before giving up.
+int wait_slot(StagingSlot& s) {
+  auto done = [&] {
+    for (uint32_t b = 0; b < s.nblocks; ++b)
+      if (__atomic_load_n(s.flags + b, __ATOMIC_ACQUIRE) != s.seq) return false;
+    return true;
+  };
+  const auto t0 = std::chrono::steady_clock::now();
+  while (!done()) {
+    if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(5)) {
+      if (hipDeviceSynchronize() != hipSuccess || !done()) return TIDE_ERR_HIP;
+      break;
+    }
+    sched_yield();
+  }
+  s.pending = false;
+  return TIDE_OK;
 }
 
 struct DeviceStaging {
@@ -89,36 +126,44 @@ int upload(const Plan& plan, void* workspace, hipStream_t stream) {
   DeviceStaging& ds = *g_staging[dev];
   StagingSlot& s = ds.slots[ds.next];
   ds.next = (ds.next + 1) % kStagingSlots;
-  if (!s.done && hipEventCreateWithFlags(&s.done, hipEventDisableTiming | hipEventDisableSystemFence) != hipSuccess)
-    return TIDE_ERR_HIP;
   if (s.pending) {
-    if (hipEventSynchronize(s.done) != hipSuccess) return TIDE_ERR_HIP;
-    s.pending = false;
+    const int rc = wait_slot(s);
+    if (rc != TIDE_OK) return rc;
   }
   const size_t need = plan.blob.size();  // a multiple of kWsAlign
   if (s.cap < need) {
     if (s.host) (void)hipHostFree(s.host);
-    s.host = nullptr;
-    s.dev = nullptr;
-    s.cap = 0;
+    if (s.flags) (void)hipHostFree(s.flags);
+    s = StagingSlot();
     size_t cap = kStagingMin;
     while (cap < need) cap *= 2;
-    if (hipHostMalloc(&s.host, cap, hipHostMallocMapped) != hipSuccess) return TIDE_ERR_HIP;
+    const size_t nflags = cap / kCopyBytesPerBlock + 1;
     void* dev_ptr = nullptr;
-    if (hipHostGetDevicePointer(&dev_ptr, s.host, 0) != hipSuccess) {
-      (void)hipHostFree(s.host);
-      s.host = nullptr;
+    void* flags_dev = nullptr;
+    if (hipHostMalloc(&s.host, cap, hipHostMallocMapped) != hipSuccess ||
+        hipHostGetDevicePointer(&dev_ptr, s.host, 0) != hipSuccess ||
+        hipHostMalloc(reinterpret_cast<void**>(&s.flags), nflags * sizeof(uint32_t),
+                      hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess ||
+        hipHostGetDevicePointer(&flags_dev, s.flags, 0) != hipSuccess) {
+      if (s.host) (void)hipHostFree(s.host);
+      if (s.flags) (void)hipHostFree(s.flags);
+      s = StagingSlot();
       return TIDE_ERR_HIP;
     }
+    memset(s.flags, 0, nflags * sizeof(uint32_t));
     s.dev = dev_ptr;
+    s.flags_dev = static_cast<uint32_t*>(flags_dev);
     s.cap = cap;
   }
   memcpy(s.host, plan.blob.data(), need);
   const size_t n16 = need / 16;
-  hipLaunchKernelGGL(stage_copy_kernel, dim3((unsigned)((n16 + 255) / 256)), dim3(256), 0, stream,
-                     static_cast<u32x4_t*>(workspace), static_cast<const u32x4_t*>(s.dev), n16);
+  const uint32_t nblocks = (uint32_t)((n16 + 255) / 256);
+  s.seq = s.seq + 1 == 0 ? 1 : s.seq + 1;  // never 0, the flags' initial value
+  hipLaunchKernelGGL(stage_copy_kernel, dim3(nblocks), dim3(256), 0, stream,
+                     static_cast<u32x4_t*>(workspace), static_cast<const u32x4_t*>(s.dev), n16,
+                     s.flags_dev, s.seq);
   if (hipGetLastError() != hipSuccess) return TIDE_ERR_HIP;
-  if (hipEventRecord(s.done, stream) != hipSuccess) return TIDE_ERR_HIP;
+  s.nblocks = nblocks;
   s.pending = true;
   return TIDE_OK;
 }
@@ -530,9 +575,9 @@ TIDE_API void tide_shutdown(void) {
   for (DeviceStaging* ds : g_staging) {
     if (!ds) continue;
     for (StagingSlot& s : ds->slots) {
-      if (s.pending && s.done) (void)hipEventSynchronize(s.done);
-      if (s.done) (void)hipEventDestroy(s.done);
+      if (s.pending) (void)wait_slot(s);
       if (s.host) (void)hipHostFree(s.host);
+      if (s.flags) (void)hipHostFree(s.flags);
     }
     delete ds;
   }
